@@ -1,0 +1,238 @@
+"""Seed-Q per-block LFSR seed search on MI355X (gfx950).
+
+Thin Python binding of libseedq.so (C ABI in ``include/seedq.h``). Every
+function of the C ABI has a wrapper of the same name that only marshals
+arguments: device buffers are torch tensors on a ROCm device, streams are torch
+streams. The compute runs in the library's HIP kernels; there is no fallback,
+and every call raises ``SeedqError`` when the library is missing or returns an
+error.
+
+Convenience helpers (``build_bases``, ``compress``, ``decompress``,
+``plan_schedule``) allocate the outputs and call the wrappers.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libseedq.so")
+
+SEEDQ_OK = 0
+SEEDQ_BLOCK = 8
+SEEDQ_MAX_RUNGS = 8
+SEEDQ_QSTRIDE = 8
+
+
+class SeedqError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {seedq_strerror(code)} ({code})" if _lib is not None
+                         else f"{where}: error {code}")
+
+
+class Rung(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("P", ctypes.c_int32)]
+
+
+class ScheduleDesc(ctypes.Structure):
+    _fields_ = [("nrows", ctypes.c_int64), ("ncols", ctypes.c_int64), ("C", ctypes.c_int32),
+                ("nrungs", ctypes.c_int32), ("rungs", ctypes.POINTER(Rung)),
+                ("damage", ctypes.POINTER(ctypes.c_double)), ("target_bpw", ctypes.c_double),
+                ("col_importance", ctypes.POINTER(ctypes.c_float)),
+                ("row_importance", ctypes.POINTER(ctypes.c_float)),
+                ("floor_fraction", ctypes.c_double)]
+
+
+class ScheduleReport(ctypes.Structure):
+    _fields_ = [("lambda_", ctypes.c_double), ("floor_q", ctypes.c_double),
+                ("tie_count", ctypes.c_int64), ("total_bits", ctypes.c_int64),
+                ("budget_bits", ctypes.c_int64), ("count", ctypes.c_int64 * SEEDQ_MAX_RUNGS),
+                ("on_hull", ctypes.c_int32 * SEEDQ_MAX_RUNGS), ("nhull", ctypes.c_int32)]
+
+
+class BasesRef(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("P", ctypes.c_int32), ("d_bases", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libseedq.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_38477_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.seedq_strerror.restype = ctypes.c_char_p
+        L.seedq_strerror.argtypes = [ctypes.c_int]
+        L.seedq_plan_schedule.restype = ctypes.c_int
+        L.seedq_plan_schedule.argtypes = [ctypes.POINTER(ScheduleDesc), vp,
+                                          ctypes.POINTER(ScheduleReport)]
+        L.seedq_bases_bytes.restype = ctypes.c_int
+        L.seedq_bases_bytes.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
+        L.seedq_build_bases.restype = ctypes.c_int
+        L.seedq_build_bases.argtypes = [i32, i32, i32, vp, vp, vp, vp]
+        L.seedq_compress_workspace_bytes.restype = sz
+        L.seedq_compress_workspace_bytes.argtypes = [i64, i64, i32, i32]
+        L.seedq_compress.restype = ctypes.c_int
+        L.seedq_compress.argtypes = [vp, i64, i64, i32, vp, i32, ctypes.POINTER(BasesRef), vp, vp,
+                                     vp, vp, vp, sz, vp]
+        L.seedq_decompress.restype = ctypes.c_int
+        L.seedq_decompress.argtypes = [vp, vp, vp, vp, i32, ctypes.POINTER(Rung), i64, i64, i32,
+                                       vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _ptr(t) -> int | None:
+    """Device (or host numpy) pointer of a buffer, None for None."""
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != SEEDQ_OK:
+        raise SeedqError(rc, where)
+
+
+# ---------------------------------------------------------------- C ABI wrappers
+
+def seedq_strerror(code: int) -> str:
+    return lib().seedq_strerror(code).decode()
+
+
+def seedq_plan_schedule(desc: ScheduleDesc, rung_of_block: np.ndarray,
+                        report: ScheduleReport | None = None) -> None:
+    assert rung_of_block.dtype == np.uint8 and rung_of_block.flags.c_contiguous
+    rc = lib().seedq_plan_schedule(ctypes.byref(desc), rung_of_block.ctypes.data,
+                                   ctypes.byref(report) if report is not None else None)
+    _check(rc, "seedq_plan_schedule")
+
+
+def seedq_bases_bytes(K: int, P: int, C: int = SEEDQ_BLOCK) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().seedq_bases_bytes(K, P, C, ctypes.byref(out)), "seedq_bases_bytes")
+    return int(out.value)
+
+
+def seedq_build_bases(K: int, P: int, C: int, d_bases, d_U=None, d_pinv=None, stream=None) -> None:
+    rc = lib().seedq_build_bases(K, P, C, _ptr(d_bases), _ptr(d_U), _ptr(d_pinv), _stream(stream))
+    _check(rc, "seedq_build_bases")
+
+
+def seedq_compress_workspace_bytes(nrows: int, ncols: int, C: int, nrungs: int) -> int:
+    return int(lib().seedq_compress_workspace_bytes(nrows, ncols, C, nrungs))
+
+
+def seedq_compress(d_W, nrows: int, ncols: int, C: int, d_rung_of_block, bases: list,
+                   d_seed, d_exp, d_q, d_err, d_workspace, workspace_bytes: int,
+                   stream=None) -> None:
+    arr = (BasesRef * len(bases))(*[BasesRef(b.K, b.P, _ptr(b.buffer)) for b in bases])
+    rc = lib().seedq_compress(_ptr(d_W), nrows, ncols, C, _ptr(d_rung_of_block), len(bases), arr,
+                              _ptr(d_seed), _ptr(d_exp), _ptr(d_q), _ptr(d_err),
+                              _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_compress")
+
+
+def seedq_decompress(d_seed, d_exp, d_q, d_rung_of_block, rungs, nrows: int, ncols: int, C: int,
+                     d_W_hat, d_acc=None, stream=None) -> None:
+    arr = (Rung * len(rungs))(*[Rung(int(K), int(P)) for K, P in rungs])
+    rc = lib().seedq_decompress(_ptr(d_seed), _ptr(d_exp), _ptr(d_q), _ptr(d_rung_of_block),
+                                len(rungs), arr, nrows, ncols, C, _ptr(d_W_hat), _ptr(d_acc),
+                                _stream(stream))
+    _check(rc, "seedq_decompress")
+
+
+# ---------------------------------------------------------------- helpers
+
+@dataclass
+class Bases:
+    """A built basis stack for rung (K, P) and its optional verification outputs."""
+    K: int
+    P: int
+    buffer: object            # torch uint8 device tensor (opaque)
+    U: object = None          # int32 [2^K-1, P, 8] or None
+    pinv: object = None       # fp32 [P, 2^K-1, 8] or None
+
+
+def plan_schedule(nrows: int, ncols: int, rungs, damage, target_bpw: float, col_importance,
+                  row_importance=None, floor_fraction: float = 0.06):
+    """Rung index per block (numpy uint8 [nblocks]) and the report as a dict."""
+    rungs = [tuple(int(v) for v in r) for r in rungs]
+    R = len(rungs)
+    rung_arr = (Rung * R)(*[Rung(K, P) for K, P in rungs])
+    dmg = None
+    if damage is not None:
+        dmg_np = np.ascontiguousarray(damage, dtype=np.float64)
+        dmg = dmg_np.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    a = np.ascontiguousarray(col_importance, dtype=np.float32)
+    rho = None if row_importance is None else np.ascontiguousarray(row_importance, dtype=np.float32)
+    desc = ScheduleDesc(nrows, ncols, SEEDQ_BLOCK, R, rung_arr, dmg, float(target_bpw),
+                        a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                        None if rho is None else rho.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                        float(floor_fraction))
+    out = np.zeros(nrows * (ncols // SEEDQ_BLOCK), dtype=np.uint8)
+    rep = ScheduleReport()
+    seedq_plan_schedule(desc, out, rep)
+    report = dict(lam=rep.lambda_, floor_q=rep.floor_q, tie_count=rep.tie_count,
+                  total_bits=rep.total_bits, budget_bits=rep.budget_bits,
+                  count=list(rep.count)[:R], on_hull=list(rep.on_hull)[:R], nhull=rep.nhull)
+    return out, report
+
+
+def build_bases(K: int, P: int, with_U: bool = False, with_pinv: bool = False, device="cuda",
+                stream=None) -> Bases:
+    import torch
+    nbytes = seedq_bases_bytes(K, P)
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    S = (1 << K) - 1
+    U = torch.empty((S, P, SEEDQ_BLOCK), dtype=torch.int32, device=device) if with_U else None
+    pinv = torch.empty((P, S, SEEDQ_BLOCK), dtype=torch.float32, device=device) if with_pinv else None
+    seedq_build_bases(K, P, SEEDQ_BLOCK, buf, U, pinv, stream)
+    return Bases(K, P, buf, U, pinv)
+
+
+def compress(W, bases: list, rung_of_block=None, with_err: bool = True, stream=None):
+    """Seed search for every block of W (torch fp32 [nrows, ncols] on the GPU).
+    Returns (seed uint32->int64 view as torch.int32, exp uint8, q int8 [nb, 8], err fp32)."""
+    import torch
+    nrows, ncols = W.shape
+    nb = nrows * ncols // SEEDQ_BLOCK
+    dev = W.device
+    seed = torch.empty(nb, dtype=torch.int32, device=dev)
+    exp = torch.empty(nb, dtype=torch.uint8, device=dev)
+    q = torch.empty((nb, SEEDQ_QSTRIDE), dtype=torch.int8, device=dev)
+    err = torch.empty(nb, dtype=torch.float32, device=dev) if with_err else None
+    nws = seedq_compress_workspace_bytes(nrows, ncols, SEEDQ_BLOCK, len(bases))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev) if nws else None
+    seedq_compress(W, nrows, ncols, SEEDQ_BLOCK, rung_of_block, bases, seed, exp, q, err, ws, nws,
+                   stream)
+    return seed, exp, q, err
+
+
+def decompress(seed, exp, q, rungs, nrows: int, ncols: int, rung_of_block=None,
+               with_acc: bool = False, stream=None):
+    import torch
+    dev = seed.device
+    W_hat = torch.empty((nrows, ncols), dtype=torch.float32, device=dev)
+    acc = torch.empty((nrows, ncols), dtype=torch.int32, device=dev) if with_acc else None
+    seedq_decompress(seed, exp, q, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK, W_hat, acc,
+                     stream)
+    return W_hat, acc

@@ -1,0 +1,120 @@
+// C ABI entry points of libseedq.so: argument checks and launches.
+#include <cstring>
+
+#include "seedq_internal.h"
+
+using namespace seedq;
+
+namespace {
+
+bool shape_ok(int64_t nrows, int64_t ncols) {
+  if (nrows <= 0 || ncols <= 0 || ncols % kC != 0) return false;
+  const int64_t G = ncols / kC;
+  return nrows <= (int64_t(1) << 31) / G && nrows * G < (int64_t(1) << 31);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* seedq_strerror(int code) {
+  switch (code) {
+    case SEEDQ_OK: return "success";
+    case SEEDQ_EINVAL: return "invalid argument (null pointer, shape, or rung count)";
+    case SEEDQ_EUNSUPPORTED: return "unsupported parameter (C must be 8, K in [8,24], P in [1,6])";
+    case SEEDQ_ERATE: return "rate budget not integral or infeasible";
+    case SEEDQ_EHULL: return "damages missing or no usable rung on the lower convex hull";
+    case SEEDQ_EHIP: return "HIP launch failed";
+    case SEEDQ_EWORKSPACE: return "workspace missing or too small";
+    default: return "unknown error";
+  }
+}
+
+int seedq_plan_schedule(const seedq_schedule_desc* desc, uint8_t* rung_of_block,
+                        seedq_schedule_report* report) {
+  return plan_schedule(desc, rung_of_block, report);
+}
+
+int seedq_bases_bytes(int32_t K, int32_t P, int32_t C, size_t* bytes) {
+  if (!bytes) return SEEDQ_EINVAL;
+  if (C != kC || !rung_supported(K, P)) return SEEDQ_EUNSUPPORTED;
+  *bytes = bases_layout(K, P).total;
+  return SEEDQ_OK;
+}
+
+int seedq_build_bases(int32_t K, int32_t P, int32_t C, void* d_bases, int32_t* d_U,
+                      float* d_pinv, void* hip_stream) {
+  if (C != kC || !rung_supported(K, P)) return SEEDQ_EUNSUPPORTED;
+  if (!d_bases || (reinterpret_cast<uintptr_t>(d_bases) & 255u)) return SEEDQ_EINVAL;
+  const hipError_t err =
+      launch_build_bases(K, P, d_bases, d_U, d_pinv, static_cast<hipStream_t>(hip_stream));
+  return err == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+size_t seedq_compress_workspace_bytes(int64_t nrows, int64_t ncols, int32_t C, int32_t nrungs) {
+  if (C != kC || !shape_ok(nrows, ncols) || nrungs <= 1 || nrungs > SEEDQ_MAX_RUNGS) return 0;
+  return compaction_workspace_bytes(nrows * (ncols / kC), nrungs);
+}
+
+int seedq_compress(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
+                   const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
+                   uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                   void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+  if (C != kC) return SEEDQ_EUNSUPPORTED;
+  if (!d_W || !bases || !d_seed || !d_exp || !d_q) return SEEDQ_EINVAL;
+  if (!shape_ok(nrows, ncols) || nrungs < 1 || nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_W) & 31u || reinterpret_cast<uintptr_t>(d_q) & 7u)
+    return SEEDQ_EINVAL;
+  for (int r = 0; r < nrungs; ++r) {
+    if (!rung_supported(bases[r].K, bases[r].P)) return SEEDQ_EUNSUPPORTED;
+    if (!bases[r].d_bases) return SEEDQ_EINVAL;
+  }
+  if (nrungs > 1 && !d_rung_of_block) return SEEDQ_EINVAL;
+  const int64_t nb = nrows * (ncols / kC);
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (nrungs == 1) {
+    const hipError_t e = launch_search(d_W, nb, nullptr, nullptr, 0, bases[0].K, bases[0].P,
+                                       bases[0].d_bases, d_seed, d_exp, d_q, d_err, stream);
+    return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+  }
+  const size_t need = compaction_workspace_bytes(nb, nrungs);
+  if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255u))
+    return SEEDQ_EWORKSPACE;
+  hipError_t e = launch_compaction(d_rung_of_block, nb, nrungs, d_workspace, d_seed, stream);
+  if (e != hipSuccess) return SEEDQ_EHIP;
+  const int32_t* list = compaction_list(d_workspace, nb, nrungs);
+  const int32_t* off = compaction_offsets(d_workspace, nb, nrungs);
+  for (int r = 0; r < nrungs; ++r) {
+    e = launch_search(d_W, nb, list, off, r, bases[r].K, bases[r].P, bases[r].d_bases, d_seed,
+                      d_exp, d_q, d_err, stream);
+    if (e != hipSuccess) return SEEDQ_EHIP;
+  }
+  return SEEDQ_OK;
+}
+
+int seedq_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+                     const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_rung* rungs,
+                     int64_t nrows, int64_t ncols, int32_t C, float* d_W_hat, int32_t* d_acc,
+                     void* hip_stream) {
+  if (C != kC) return SEEDQ_EUNSUPPORTED;
+  if (!d_seed || !d_exp || !d_q || !rungs || !d_W_hat) return SEEDQ_EINVAL;
+  if (!shape_ok(nrows, ncols) || nrungs < 1 || nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
+  if (nrungs > 1 && !d_rung_of_block) return SEEDQ_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_q) & 7u || reinterpret_cast<uintptr_t>(d_W_hat) & 15u ||
+      reinterpret_cast<uintptr_t>(d_acc) & 15u)
+    return SEEDQ_EINVAL;
+  RungTable rt;
+  std::memset(&rt, 0, sizeof(rt));
+  rt.n = nrungs;
+  for (int r = 0; r < nrungs; ++r) {
+    if (!rung_supported(rungs[r].K, rungs[r].P)) return SEEDQ_EUNSUPPORTED;
+    rt.K[r] = rungs[r].K;
+    rt.P[r] = rungs[r].P;
+  }
+  const hipError_t e = launch_decompress(d_seed, d_exp, d_q, nrungs > 1 ? d_rung_of_block : nullptr,
+                                         rt, nrows * (ncols / kC), d_W_hat, d_acc,
+                                         static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+}  // extern "C"

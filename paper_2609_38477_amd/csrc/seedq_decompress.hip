@@ -1,0 +1,74 @@
+// Reconstruction w_hat = U(s) q 2^-e (Algorithm 2; the appendix on cost: one
+// LFSR expansion and k_b multiply-accumulates per weight).
+//
+// One thread per block: it regenerates the 8P LFSR states of its seed, forms
+// the exact integer reconstruction acc_i = sum_j U_int[i][j] q_j (|acc| < 2^29)
+// and scales it by 2^-(K-1+e) after a single rounding to fp32. Reads 14 bytes
+// of code per block, writes 32 bytes of weights (+32 of acc); neighbouring
+// threads touch neighbouring 32-byte blocks, so every access is coalesced.
+#include "seedq_internal.h"
+
+namespace seedq {
+namespace {
+
+__global__ void __launch_bounds__(256)
+decompress_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
+                  const int8_t* __restrict__ q, const uint8_t* __restrict__ rung, RungTable rt,
+                  int64_t nblocks, float* __restrict__ W_hat, int32_t* __restrict__ acc_out) {
+  const int64_t b = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (b >= nblocks) return;
+  const int r = rung ? int(rung[b]) : 0;
+  bool ok = r < rt.n;
+  const int K = ok ? rt.K[r] : SEEDQ_MIN_K;
+  const int P = ok ? rt.P[r] : 1;
+  const uint32_t s = seed[b];
+  const int e = expo[b];
+  ok = ok && s >= 1u && s < (1u << K) && e <= 15;
+  const uint2 qw = reinterpret_cast<const uint2*>(q)[b];
+  const uint32_t mask = lfsr_mask(K);
+  const int32_t half = int32_t(1) << (K - 1);
+
+  int32_t acc[kC];
+#pragma unroll
+  for (int i = 0; i < kC; ++i) acc[i] = 0;
+  uint32_t x = s;
+  for (int j = 0; j < P; ++j) {
+    const uint32_t word = (j < 4) ? qw.x : qw.y;
+    const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      acc[i] += (int32_t(x) - half) * qj;
+      x = lfsr_step(x, mask);
+    }
+  }
+  const int sh = -(K - 1 + e);
+  float o[kC];
+#pragma unroll
+  for (int i = 0; i < kC; ++i) {
+    o[i] = ok ? ldexpf(__int2float_rn(acc[i]), sh) : __int_as_float(0x7fc00000);
+    if (!ok) acc[i] = 0;
+  }
+  float4* dst = reinterpret_cast<float4*>(W_hat + b * kC);
+  dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+  dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+  if (acc_out) {
+    int4* da = reinterpret_cast<int4*>(acc_out + b * kC);
+    da[0] = make_int4(acc[0], acc[1], acc[2], acc[3]);
+    da[1] = make_int4(acc[4], acc[5], acc[6], acc[7]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+                             const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
+                             float* d_W_hat, int32_t* d_acc, hipStream_t stream) {
+  if (nblocks == 0) return hipSuccess;
+  const int threads = 256;
+  const int64_t blocks = (nblocks + threads - 1) / threads;
+  hipLaunchKernelGGL(decompress_kernel, dim3(unsigned(blocks)), dim3(threads), 0, stream, d_seed,
+                     d_exp, d_q, d_rung, rt, nblocks, d_W_hat, d_acc);
+  return hipGetLastError();
+}
+
+}  // namespace seedq

@@ -1,0 +1,103 @@
+// Internal declarations shared by the translation units of libseedq.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "seedq.h"
+
+namespace seedq {
+
+constexpr int kC = 8;            // weights per block (section 3.1, B = 8)
+constexpr int kMaxP = SEEDQ_MAX_P;
+
+// Feedback masks of maximal-length Galois LFSRs, K = 8 .. 24 (bit K-1 set).
+// Right-shift Galois form: x <- (x >> 1) ^ (x odd ? mask : 0).
+__host__ __device__ inline uint32_t lfsr_mask(int K) {
+  switch (K) {
+    case 8: return 0xB8u;
+    case 9: return 0x110u;
+    case 10: return 0x240u;
+    case 11: return 0x500u;
+    case 12: return 0x829u;
+    case 13: return 0x100Du;
+    case 14: return 0x2015u;
+    case 15: return 0x6000u;
+    case 16: return 0xD008u;
+    case 17: return 0x12000u;
+    case 18: return 0x20400u;
+    case 19: return 0x40023u;
+    case 20: return 0x90000u;
+    case 21: return 0x140000u;
+    case 22: return 0x300000u;
+    case 23: return 0x420000u;
+    case 24: return 0xE10000u;
+    default: return 0u;
+  }
+}
+
+__host__ __device__ __forceinline__ uint32_t lfsr_step(uint32_t x, uint32_t mask) {
+  return (x >> 1) ^ ((0u - (x & 1u)) & mask);
+}
+
+// Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
+//   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
+//   q32:    float  [S][P][8]   orthonormal basis of range(U(s)) (rows of Q^T);
+//                               rows beyond the rank are zero
+struct BasesLayout {
+  int64_t nseeds;
+  size_t off_pinv64, off_q32, total;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline BasesLayout bases_layout(int K, int P) {
+  BasesLayout L;
+  L.nseeds = (int64_t(1) << K) - 1;
+  L.off_pinv64 = 0;
+  L.off_q32 = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
+  L.total = align256(L.off_q32 + size_t(L.nseeds) * P * kC * sizeof(float));
+  return L;
+}
+
+inline bool rung_supported(int K, int P) {
+  return K >= SEEDQ_MIN_K && K <= SEEDQ_MAX_K && P >= 1 && P <= kMaxP;
+}
+
+// Rung table passed to kernels by value.
+struct RungTable {
+  int32_t n;
+  int32_t K[SEEDQ_MAX_RUNGS];
+  int32_t P[SEEDQ_MAX_RUNGS];
+};
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_build_bases(int K, int P, void* d_bases, int32_t* d_U, float* d_pinv,
+                              hipStream_t stream);
+
+// Deterministic, order-preserving split of the blocks by rung:
+// lists: int32 [nblocks] (the per-rung lists back to back), meta: see .hip.
+size_t compaction_workspace_bytes(int64_t nblocks, int nrungs);
+hipError_t launch_compaction(const uint8_t* d_rung, int64_t nblocks, int nrungs, void* d_ws,
+                             uint32_t* d_seed_invalid, hipStream_t stream);
+// Device pointers into the workspace after launch_compaction.
+const int32_t* compaction_list(void* d_ws, int64_t nblocks, int nrungs);
+const int32_t* compaction_offsets(void* d_ws, int64_t nblocks, int nrungs);
+
+// Search over all seeds of rung (K, P) for the blocks listed at
+// list[off[r] .. off[r+1]) (list == nullptr: all nblocks blocks in order).
+hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                         const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
+                         uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                         hipStream_t stream);
+
+hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+                             const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
+                             float* d_W_hat, int32_t* d_acc, hipStream_t stream);
+
+// Host planner (seedq_schedule.cpp).
+int plan_schedule(const seedq_schedule_desc* desc, uint8_t* rung_of_block,
+                  seedq_schedule_report* report);
+
+}  // namespace seedq

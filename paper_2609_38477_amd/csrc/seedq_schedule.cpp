@@ -1,0 +1,314 @@
+// Host planner for the rung schedule (sections 3.2-3.4, Algorithms 1-2).
+//
+// Importance (eq. (imp)): imp_b = abar_g * rho_r, abar_g the mean of the fp32
+// column importances a_j over the block's 8 columns, both factors normalised to
+// unit mean; every sum runs in index order in fp64 (appendix "Agreement").
+// Floor (section 3.3): q = sorted(imp)[ceil(f * nblocks) - 1], imp <- max(imp, q).
+// Hull (section 3.4): lower convex hull of (rate, damage) over the rungs, slopes
+// s_j = (e_j - e_{j+1}) / (r_{j+1} - r_j) in bits per weight.
+// Ladder (eq. (ladder)): a block of importance v sits at hull position
+// |{j : fl(lambda / s_j) <= v}|.
+//
+// Instead of bisecting on lambda, the planner sweeps the exact breakpoints of
+// that ladder: for every distinct importance v and hull step j, the largest
+// double lambda with fl(lambda / s_j) <= v. Walking the breakpoints from the
+// largest down promotes whole groups of equally important blocks; the first
+// group that does not fit is the tied group of the tie pass, demoted in
+// row-major block order until the budget is met (Algorithm 2: the first T_t
+// tied blocks take the lower rung). The result equals bisection plus the tie
+// pass (Everett's theorem), without floating-point search.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "seedq_internal.h"
+
+namespace seedq {
+namespace {
+
+struct Breakpoint {
+  double lam;
+  int cls;   // importance class
+  int step;  // hull step j (promotion from position j to j + 1)
+};
+
+// Largest lambda >= 0 with fl(lambda / s) <= v (v > 0, s > 0).
+double breakpoint(double v, double s) {
+  double lam = v * s;
+  while (lam > 0.0 && lam / s > v) lam = std::nextafter(lam, 0.0);
+  for (;;) {
+    const double up = std::nextafter(lam, INFINITY);
+    if (std::isfinite(up) && up / s <= v) lam = up;
+    else break;
+  }
+  return lam;
+}
+
+}  // namespace
+
+int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_report* rep) {
+  if (!d || !rob || !d->rungs || !d->col_importance) return SEEDQ_EINVAL;
+  if (d->C != kC) return SEEDQ_EUNSUPPORTED;
+  if (d->nrows <= 0 || d->ncols <= 0 || d->ncols % kC != 0) return SEEDQ_EINVAL;
+  if (d->nrungs < 1 || d->nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
+  const int R = d->nrungs;
+  for (int r = 0; r < R; ++r)
+    if (!rung_supported(d->rungs[r].K, d->rungs[r].P)) return SEEDQ_EUNSUPPORTED;
+  if (R > 1) {
+    if (!d->damage) return SEEDQ_EHULL;
+    for (int r = 0; r < R; ++r)
+      if (!std::isfinite(d->damage[r])) return SEEDQ_EHULL;
+  }
+  if (!(d->floor_fraction >= 0.0 && d->floor_fraction < 1.0)) return SEEDQ_EINVAL;
+  const int64_t nrows = d->nrows, G = d->ncols / kC;
+  if (nrows > (int64_t(1) << 40) / G) return SEEDQ_EINVAL;
+  const int64_t nb = nrows * G;
+
+  const double budget_f = 8.0 * d->target_bpw * double(nb);
+  if (!std::isfinite(budget_f) || budget_f < 0.0 || budget_f >= 9.0e18 ||
+      budget_f != std::floor(budget_f))
+    return SEEDQ_ERATE;
+  const int64_t budget = int64_t(budget_f);
+
+  std::vector<double> bits(R);
+  for (int r = 0; r < R; ++r) bits[r] = double(d->rungs[r].K + 4 * d->rungs[r].P + 4);
+
+  // ---- importance (eq. (imp)), fixed evaluation order
+  std::vector<double> abar(G);
+  for (int64_t g = 0; g < G; ++g) {
+    double s = 0.0;
+    for (int j = 0; j < kC; ++j) {
+      const double a = double(d->col_importance[g * kC + j]);
+      if (!(a > 0.0) || !std::isfinite(a)) return SEEDQ_EINVAL;
+      s = s + a;
+    }
+    abar[g] = s / 8.0;
+  }
+  double tot = 0.0;
+  for (int64_t g = 0; g < G; ++g) tot = tot + abar[g];
+  const double amean = tot / double(G);
+  for (int64_t g = 0; g < G; ++g) abar[g] = abar[g] / amean;
+  std::vector<double> rho;
+  if (d->row_importance) {
+    rho.resize(nrows);
+    double tr = 0.0;
+    for (int64_t r = 0; r < nrows; ++r) {
+      const double v = double(d->row_importance[r]);
+      if (!(v > 0.0) || !std::isfinite(v)) return SEEDQ_EINVAL;
+      tr = tr + v;
+    }
+    const double rmean = tr / double(nrows);
+    for (int64_t r = 0; r < nrows; ++r) rho[r] = double(d->row_importance[r]) / rmean;
+  }
+  auto imp_of = [&](int64_t b) -> double {
+    const double a = abar[b % G];
+    return rho.empty() ? 1.0 * a : rho[b / G] * a;
+  };
+
+  // ---- floor (section 3.3)
+  int64_t kq = int64_t(std::ceil(double(nb) * d->floor_fraction)) - 1;
+  if (kq < 0) kq = 0;
+  if (kq > nb - 1) kq = nb - 1;
+  double qf;
+  if (rho.empty()) {
+    std::vector<double> sg(abar);
+    std::sort(sg.begin(), sg.end());
+    qf = 1.0 * sg[kq / nrows];
+  } else {
+    std::vector<double> all(nb);
+    for (int64_t b = 0; b < nb; ++b) all[b] = imp_of(b);
+    std::nth_element(all.begin(), all.begin() + kq, all.end());
+    qf = all[kq];
+  }
+
+  // ---- importance classes: equal floored importance
+  // cls_of_group (rho == 1) or cls_of_block (general); members listed in block order
+  std::vector<double> cls_val;
+  std::vector<int64_t> cls_count;
+  std::vector<int32_t> cls_of;  // per group (rho == 1) or per block
+  {
+    const int64_t n = rho.empty() ? G : nb;
+    std::vector<int64_t> idx(n);
+    for (int64_t i = 0; i < n; ++i) idx[i] = i;
+    auto val = [&](int64_t i) { return std::max(rho.empty() ? 1.0 * abar[i] : imp_of(i), qf); };
+    std::vector<double> v(n);
+    for (int64_t i = 0; i < n; ++i) v[i] = val(i);
+    std::sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
+      return v[a] < v[b] || (v[a] == v[b] && a < b);
+    });
+    cls_of.assign(n, -1);
+    for (int64_t k = 0; k < n; ++k) {
+      const int64_t i = idx[k];
+      if (cls_val.empty() || v[i] != cls_val.back()) {
+        cls_val.push_back(v[i]);
+        cls_count.push_back(0);
+      }
+      cls_of[i] = int32_t(cls_val.size() - 1);
+      cls_count.back() += rho.empty() ? nrows : 1;
+    }
+  }
+  const int ncls = int(cls_val.size());
+
+  // ---- hull (section 3.4)
+  std::vector<int> H;
+  if (R == 1) {
+    H.push_back(0);
+  } else {
+    std::vector<int> order(R);
+    for (int r = 0; r < R; ++r) order[r] = r;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+      if (bits[a] != bits[b]) return bits[a] < bits[b];
+      if (d->damage[a] != d->damage[b]) return d->damage[a] < d->damage[b];
+      return a < b;
+    });
+    for (int i : order) {
+      if (!H.empty() && bits[H.back()] == bits[i]) continue;
+      while (H.size() >= 2) {
+        const int a = H[H.size() - 2], b = H.back();
+        const double cross = (bits[b] - bits[a]) * (d->damage[i] - d->damage[a]) -
+                             (d->damage[b] - d->damage[a]) * (bits[i] - bits[a]);
+        if (cross <= 0.0) H.pop_back();
+        else break;
+      }
+      H.push_back(i);
+    }
+    while (H.size() >= 2 && d->damage[H.back()] >= d->damage[H[H.size() - 2]]) H.pop_back();
+  }
+  const int J = int(H.size());
+  if (J < 1) return SEEDQ_EHULL;
+  std::vector<double> slope(J > 1 ? J - 1 : 0);
+  for (int j = 0; j + 1 < J; ++j)
+    slope[j] = (d->damage[H[j]] - d->damage[H[j + 1]]) / ((bits[H[j + 1]] - bits[H[j]]) / 8.0);
+
+  if (double(nb) * bits[H[0]] > double(budget)) return SEEDQ_ERATE;
+
+  // ---- breakpoint sweep
+  std::vector<int> level(ncls, 0);
+  std::vector<Breakpoint> ev;
+  ev.reserve(size_t(ncls) * (J > 1 ? J - 1 : 0));
+  for (int c = 0; c < ncls; ++c)
+    for (int j = 0; j + 1 < J; ++j) ev.push_back({breakpoint(cls_val[c], slope[j]), c, j});
+  std::sort(ev.begin(), ev.end(), [](const Breakpoint& a, const Breakpoint& b) {
+    if (a.lam != b.lam) return a.lam > b.lam;
+    if (a.cls != b.cls) return a.cls < b.cls;
+    return a.step < b.step;
+  });
+
+  int64_t total = nb * int64_t(bits[H[0]]);
+  double lam = 0.0;
+  int64_t T = 0;
+  // tied group (if any): classes promoted at the final threshold, and how many
+  // of their blocks (in block order) keep the lower position
+  std::vector<int> tied_cls;
+  std::vector<int> tied_from;  // position before the threshold, per tied class
+  size_t k = 0;
+  bool done = false;
+  while (k < ev.size() && !done) {
+    size_t k1 = k;
+    while (k1 < ev.size() && ev[k1].lam == ev[k].lam) ++k1;
+    const double lk = ev[k].lam;
+    if (total == budget) {
+      lam = std::nextafter(lk, INFINITY);
+      done = true;
+      break;
+    }
+    int64_t delta = 0;
+    for (size_t t = k; t < k1; ++t) {
+      const int c = ev[t].cls, j = ev[t].step;
+      delta += cls_count[c] * int64_t(bits[H[j + 1]] - bits[H[j]]);
+    }
+    if (total + delta <= budget) {
+      for (size_t t = k; t < k1; ++t) level[ev[t].cls] = ev[t].step + 1;
+      total += delta;
+      k = k1;
+      continue;
+    }
+    // tie pass over the classes promoted at lk
+    std::vector<int> from_of(ncls, -1);
+    for (size_t t = k; t < k1; ++t) {
+      const int c = ev[t].cls;
+      if (from_of[c] < 0) {
+        from_of[c] = level[c];
+        tied_cls.push_back(c);
+      }
+    }
+    std::sort(tied_cls.begin(), tied_cls.end());
+    std::vector<int> to_of(ncls, -1);
+    for (size_t t = k; t < k1; ++t) to_of[ev[t].cls] = std::max(to_of[ev[t].cls], ev[t].step + 1);
+    int64_t cur = total + delta;
+    int64_t members = 0;
+    for (int c : tied_cls) members += cls_count[c];
+    // demote members in block order until the budget is met
+    auto gain = [&](int c) {
+      return int64_t(bits[H[to_of[c]]] - bits[H[from_of[c]]]);
+    };
+    T = 0;
+    if (rho.empty()) {
+      // block order over the tied groups: rows outer, groups inner
+      std::vector<int64_t> groups;
+      for (int64_t g = 0; g < G; ++g)
+        if (from_of[cls_of[g]] >= 0) groups.push_back(g);
+      for (int64_t r = 0; r < nrows && cur > budget; ++r)
+        for (size_t gi = 0; gi < groups.size() && cur > budget; ++gi) {
+          cur -= gain(cls_of[groups[gi]]);
+          ++T;
+        }
+    } else {
+      for (int64_t b = 0; b < nb && cur > budget; ++b) {
+        const int c = cls_of[b];
+        if (from_of[c] >= 0) {
+          cur -= gain(c);
+          ++T;
+        }
+      }
+    }
+    if (T == members) {
+      lam = std::nextafter(lk, INFINITY);
+      T = 0;
+      tied_cls.clear();
+    } else {
+      lam = lk;
+      for (int c : tied_cls) {
+        tied_from.push_back(from_of[c]);
+        level[c] = to_of[c];
+      }
+      total = cur;
+    }
+    done = true;
+  }
+  if (!done) lam = 0.0;
+
+  // ---- write the allocation
+  int64_t count[SEEDQ_MAX_RUNGS] = {0};
+  std::vector<int> cls_tied_from(ncls, -1);
+  for (size_t t = 0; t < tied_cls.size(); ++t) cls_tied_from[tied_cls[t]] = tied_from[t];
+  int64_t demote_left = T;
+  int64_t check_total = 0;
+  for (int64_t b = 0; b < nb; ++b) {
+    const int c = rho.empty() ? cls_of[b % G] : cls_of[b];
+    int pos = level[c];
+    if (cls_tied_from[c] >= 0 && demote_left > 0) {
+      pos = cls_tied_from[c];
+      --demote_left;
+    }
+    const int rr = H[pos];
+    rob[b] = uint8_t(rr);
+    count[rr] += 1;
+    check_total += int64_t(bits[rr]);
+  }
+  if (rep) {
+    std::memset(rep, 0, sizeof(*rep));
+    rep->lambda = lam;
+    rep->floor_q = qf;
+    rep->tie_count = T;
+    rep->total_bits = check_total;
+    rep->budget_bits = budget;
+    for (int r = 0; r < R; ++r) rep->count[r] = count[r];
+    for (int j = 0; j < J; ++j) rep->on_hull[H[j]] = 1;
+    rep->nhull = J;
+  }
+  return SEEDQ_OK;
+}
+
+}  // namespace seedq

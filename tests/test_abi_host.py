@@ -1,0 +1,146 @@
+"""Host-side checks of libseedq.so: every symbol the header declares is
+exported, argument errors are reported without touching a GPU, and the host
+rung planner matches the oracle's allocation exactly."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synthetic
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "seedq.h")
+
+
+@pytest.fixture(scope="module")
+def sq():
+    import paper_2609_38477_amd as sq
+    if not os.path.exists(sq.LIB_PATH):
+        from paper_2609_38477_amd import build
+        build.build()
+    return sq
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(seedq_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(sq):
+    names = _declared()
+    assert len(names) == 7
+    L = ctypes.CDLL(sq.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror(sq):
+    assert "success" in sq.seedq_strerror(0)
+    for c in range(-6, 0):
+        assert sq.seedq_strerror(c) != sq.seedq_strerror(0)
+
+
+def test_bases_bytes_and_errors(sq):
+    n = sq.seedq_bases_bytes(16, 3)
+    assert n >= (2 ** 16 - 1) * 3 * 8 * (8 + 4)
+    assert n % 256 == 0
+    for K, P, C in [(7, 3, 8), (25, 3, 8), (12, 0, 8), (12, 7, 8), (12, 3, 4)]:
+        with pytest.raises(sq.SeedqError) as e:
+            sq.seedq_bases_bytes(K, P, C)
+        assert e.value.code == -2
+
+
+def test_compress_argument_errors_need_no_gpu(sq):
+    L = sq.lib()
+    b = (sq.BasesRef * 1)(sq.BasesRef(16, 3, 256))
+    # null weights
+    assert L.seedq_compress(None, 8, 8, 8, None, 1, b, 256, 256, 256, None, None, 0, None) == -1
+    # ncols not a multiple of 8
+    assert L.seedq_compress(256, 8, 12, 8, None, 1, b, 256, 256, 256, None, None, 0, None) == -1
+    # C != 8
+    assert L.seedq_compress(256, 8, 8, 4, None, 1, b, 256, 256, 256, None, None, 0, None) == -2
+    # several rungs without a rung array
+    b2 = (sq.BasesRef * 2)(sq.BasesRef(12, 2, 256), sq.BasesRef(16, 3, 256))
+    assert L.seedq_compress(256, 8, 8, 8, None, 2, b2, 256, 256, 256, None, None, 0, None) == -1
+    # workspace too small
+    assert L.seedq_compress(256, 8, 8, 8, 256, 2, b2, 256, 256, 256, None, None, 0, None) == -6
+    # unsupported rung
+    b3 = (sq.BasesRef * 1)(sq.BasesRef(30, 3, 256))
+    assert L.seedq_compress(256, 8, 8, 8, None, 1, b3, 256, 256, 256, None, None, 0, None) == -2
+    assert sq.seedq_compress_workspace_bytes(4096, 4096, 8, 1) == 0
+    assert sq.seedq_compress_workspace_bytes(4096, 4096, 8, 3) >= 4 * 4096 * 512
+
+
+def _compare(sq, oq, nrows, ncols, rungs, damage, target, a, rho=None, f=0.06):
+    mine, rep = sq.plan_schedule(nrows, ncols, rungs, damage, target, a, rho, f)
+    ref = oq.schedule(nrows, ncols, rungs, damage, target, a, rho, f)
+    assert np.array_equal(mine, ref.rung_of_block)
+    assert rep["tie_count"] == ref.tie_count
+    assert rep["lam"] == ref.lam
+    assert rep["floor_q"] == ref.floor_q
+    assert rep["total_bits"] == ref.total_bits
+    assert rep["budget_bits"] == ref.budget_bits
+    return mine, rep, ref
+
+
+@pytest.mark.parametrize("name", ["mlp_up", "reduced", "l70b", "attn4096"])
+def test_planner_matches_oracle_on_workload_shapes(sq, oq, name):
+    wl = synthetic.WORKLOADS[name]
+    a = synthetic.importance_profile(wl.ncols)
+    mine, rep, ref = _compare(sq, oq, 16, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
+    assert rep["total_bits"] == rep["budget_bits"]
+
+
+def test_planner_full_size_rate_identity(sq):
+    # the full 8192 x 28672 layer: rate identity and the expected split
+    wl = synthetic.WORKLOADS["l70b"]
+    a = synthetic.importance_profile(wl.ncols)
+    rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
+    bits = np.array([K + 4 * P + 4 for K, P in wl.rungs])
+    assert int(bits[rob].sum()) == rep["total_bits"] == rep["budget_bits"] == 32 * wl.nblocks
+    frac = np.bincount(rob, minlength=3) / rob.size
+    assert np.allclose(frac, [0.2441, 0.5117, 0.2441], atol=5e-4)
+
+
+@pytest.mark.parametrize("trial", range(12))
+def test_planner_matches_oracle_random(sq, oq, trial):
+    rng = np.random.default_rng(100 + trial)
+    nrows = int(rng.integers(1, 6))
+    ncols = 8 * int(rng.integers(1, 12))
+    a = np.exp(rng.normal(0, 1, ncols)).astype(np.float32)
+    if trial % 3 == 0:
+        a = np.round(a * 4).clip(1) .astype(np.float32)      # many exact ties between groups
+    rho = np.exp(rng.normal(0, 0.5, nrows)).astype(np.float32) if trial % 2 else None
+    nb = nrows * ncols // 8
+    rungs = ((12, 2), (16, 3), (20, 4))
+    damage = (4.0, 1.0, 0.25)
+    lo, hi = 24 * nb, 40 * nb
+    target = float(rng.integers(lo // 8, hi // 8 + 1)) * 8 / (8 * nb)
+    _compare(sq, oq, nrows, ncols, rungs, damage, target, a, rho, f=float(rng.choice([0.0, 0.06, 0.3])))
+
+
+def test_planner_tie_split(sq, oq):
+    a = synthetic.importance_profile(32)
+    nb = 12
+    mine, rep, ref = _compare(sq, oq, 3, 32, ((12, 2), (16, 3), (20, 4)), (4.0, 1.0, 0.25),
+                              (24 * nb + 40) / (8 * nb), a, f=0.0)
+    assert rep["tie_count"] > 0
+
+
+def test_planner_errors(sq):
+    a = synthetic.importance_profile(64)
+    with pytest.raises(sq.SeedqError) as e:
+        sq.plan_schedule(4, 64, ((12, 2), (16, 3)), (4.0, 1.0), 2.0, a)   # below lowest rate
+    assert e.value.code == -3
+    with pytest.raises(sq.SeedqError) as e:
+        sq.plan_schedule(3, 8, ((12, 2), (16, 3)), (4.0, 1.0), 3.3, a[:8])  # 8*3.3*3 not integral
+    assert e.value.code == -3
+    with pytest.raises(sq.SeedqError) as e:
+        sq.plan_schedule(4, 64, ((12, 2), (16, 3)), None, 3.5, a)
+    assert e.value.code == -4
+    with pytest.raises(sq.SeedqError) as e:
+        sq.plan_schedule(4, 60, ((12, 2),), None, 3.0, a[:60])
+    assert e.value.code == -1
