@@ -13,11 +13,13 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libseedq.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
-HIP_SOURCES = ["seedq_bases.hip", "seedq_search.hip", "seedq_compact.hip", "seedq_decompress.hip"]
+HIP_SOURCES = ["seedq_bases.hip", "seedq_search.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
+               "seedq_decompress.hip"]
 HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp"]
 
 # Device code is compiled without packed fp32 instructions.
-DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC, "-Wall", "-Wno-unused-function"]
 
 

@@ -41,13 +41,30 @@ __host__ __device__ __forceinline__ uint32_t lfsr_step(uint32_t x, uint32_t mask
   return (x >> 1) ^ ((0u - (x & 1u)) & mask);
 }
 
+// The least-squares residual bound of the search is a quadratic form in the
+// block: ||Q_s^T w||^2 = w^T Pi_s w = sum over pairs i <= j of Pi_s[i][j] z_ij,
+// z_ij = c_ij w_i w_j (c = 1 on the diagonal, 2 off it). The 36 pairs, padded
+// to 48, form the reduction dimension of three 32x32x16 fp16 MFMAs.
+constexpr int kPairs = 36;
+constexpr int kPairsPadded = 48;
+constexpr int kSeedTile = 32;                   // seeds per MFMA tile (rows)
+constexpr float kOperandScale = 4096.0f;        // 2^12 on both fp16 operands
+constexpr int kTileBytes = kPairsPadded * kSeedTile * 2;   // 3 KB per seed tile
+
+// Pair index k of (i, j), i <= j, row-major over the upper triangle.
+__host__ __device__ constexpr int pair_index(int i, int j) { return i * kC - i * (i - 1) / 2 + (j - i); }
+
 // Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
 //   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
 //   q32:    float  [S][P][8]   orthonormal basis of range(U(s)) (rows of Q^T);
 //                               rows beyond the rank are zero
+//   pi16:   fp16 [ntiles][3][64][8]  2^12 Pi_s[k] as MFMA A-operand fragments:
+//           tile T holds seeds 32T+1 .. 32T+32; fragment t, lane l, element e
+//           is pair k = 16t + 8(l/32) + e of seed 32T + (l%32) + 1 (zero for
+//           k >= 36 and for seeds beyond 2^K - 1)
 struct BasesLayout {
-  int64_t nseeds;
-  size_t off_pinv64, off_q32, total;
+  int64_t nseeds, ntiles;
+  size_t off_pinv64, off_q32, off_pi16, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -55,9 +72,11 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline BasesLayout bases_layout(int K, int P) {
   BasesLayout L;
   L.nseeds = (int64_t(1) << K) - 1;
+  L.ntiles = (L.nseeds + kSeedTile - 1) / kSeedTile;
   L.off_pinv64 = 0;
   L.off_q32 = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
-  L.total = align256(L.off_q32 + size_t(L.nseeds) * P * kC * sizeof(float));
+  L.off_pi16 = align256(L.off_q32 + size_t(L.nseeds) * P * kC * sizeof(float));
+  L.total = align256(L.off_pi16 + size_t(L.ntiles) * kTileBytes);
   return L;
 }
 
@@ -91,6 +110,15 @@ hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_lis
                          const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
                          uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
                          hipStream_t stream);
+
+hipError_t launch_search_valu(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                              const int32_t* d_off, int rung_index, int K, int P,
+                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
+                              float* d_err, hipStream_t stream);
+hipError_t launch_search_mfma(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                              const int32_t* d_off, int rung_index, int K, int P,
+                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
+                              float* d_err, hipStream_t stream);
 
 hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
                              const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,

@@ -13,67 +13,13 @@
 // states, and the fp64 sum of squares in index order. Seeds are visited in
 // increasing order and only a strictly smaller error replaces the best, so
 // ties go to the smallest seed.
+#include <cstdlib>
+#include <cstring>
+
+#include "seedq_exact.h"
 #include "seedq_internal.h"
 
 namespace seedq {
-
-// ------------------------------------------------------------ exact evaluation
-
-// Quantised error of seed s for block w (fp64, exact reconstruction).
-// A: pinv(U(s)), P x 8 row-major (fp64).
-template <int P>
-__device__ __forceinline__ double exact_eval(const float (&w)[kC], const double* __restrict__ A,
-                                             uint32_t s, int K, uint32_t mask, int& e_out,
-                                             int (&q)[P]) {
-#pragma clang fp contract(off)
-  double t[P];
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    double acc = 0.0;
-#pragma unroll
-    for (int i = 0; i < kC; ++i) acc = acc + A[p * kC + i] * double(w[i]);
-    t[p] = acc;
-  }
-  // largest e in [0, 15] at which every rne(t_p 2^e) lies in [-8, 7]
-  int e = 15;
-  for (; e >= 0; --e) {
-    bool fits = true;
-#pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const double r = rint(ldexp(t[p], e));
-      fits = fits && (r <= 7.0) && (r >= -8.0);
-    }
-    if (fits) break;
-  }
-  if (e < 0) e = 0;
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    const double r = fmin(fmax(rint(ldexp(t[p], e)), -8.0), 7.0);
-    q[p] = int(r);
-  }
-  const int32_t half = int32_t(1) << (K - 1);
-  int32_t acc[kC];
-#pragma unroll
-  for (int i = 0; i < kC; ++i) acc[i] = 0;
-  uint32_t x = s;
-#pragma unroll
-  for (int j = 0; j < P; ++j) {
-#pragma unroll
-    for (int i = 0; i < kC; ++i) {
-      acc[i] += (int32_t(x) - half) * q[j];
-      x = lfsr_step(x, mask);
-    }
-  }
-  const int sh = -(K - 1 + e);
-  double err = 0.0;
-#pragma unroll
-  for (int i = 0; i < kC; ++i) {
-    const double d = double(w[i]) - ldexp(double(acc[i]), sh);
-    err = err + d * d;
-  }
-  e_out = e;
-  return err;
-}
 
 // ------------------------------------------------------------ VALU search kernel
 
@@ -188,10 +134,10 @@ hipError_t launch_search_p(const float* d_W, int64_t nblocks, const int32_t* d_l
   return hipGetLastError();
 }
 
-hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_list,
-                         const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
-                         uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
-                         hipStream_t stream) {
+hipError_t launch_search_valu(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                              const int32_t* d_off, int rung_index, int K, int P,
+                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
+                              float* d_err, hipStream_t stream) {
   switch (P) {
 #define SEEDQ_CASE(PP)                                                                       \
   case PP:                                                                                   \
@@ -206,6 +152,27 @@ hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_lis
 #undef SEEDQ_CASE
     default: return hipErrorInvalidValue;
   }
+}
+
+// Engine selection: the matrix-core engine by default; SEEDQ_ENGINE=valu picks
+// the one-thread-per-block vector engine (same results, used to cross-check).
+static bool use_valu_engine() {
+  static const bool v = [] {
+    const char* e = std::getenv("SEEDQ_ENGINE");
+    return e && std::strcmp(e, "valu") == 0;
+  }();
+  return v;
+}
+
+hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                         const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
+                         uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                         hipStream_t stream) {
+  if (use_valu_engine())
+    return launch_search_valu(d_W, nblocks, d_list, d_off, rung_index, K, P, d_bases, d_seed,
+                              d_exp, d_q, d_err, stream);
+  return launch_search_mfma(d_W, nblocks, d_list, d_off, rung_index, K, P, d_bases, d_seed, d_exp,
+                            d_q, d_err, stream);
 }
 
 }  // namespace seedq

@@ -1,0 +1,400 @@
+// Matrix-core engine of the per-block exhaustive seed search (section 3.1;
+// per the appendix on cost, 2^K least-squares fits per block dominate the
+// encoder).
+//
+// Screen. For block w and seed s the least-squares residual
+//     r_LS(s) = ||w||^2 - w^T Pi_s w,        Pi_s = projector onto range(U(s)),
+// is a lower bound on every quantised error of that seed. w^T Pi_s w is linear
+// in the 36 products z_ij = c_ij w_i w_j (i <= j), so the bounds of 32 seeds x
+// 32 blocks are one [32 x 48] x [48 x 32] product: three
+// v_mfma_f32_32x32x16_f16 with fp16 operands (2^12-scaled projector entries
+// from the basis stack, 2^12-scaled pair products of the block) and fp32
+// accumulation. A candidate passes when its bound can be at most the block's
+// best error so far; the fp16 rounding of the operands is covered by the
+// margin gamma = sqrt(P) 2^-10 (1 + 2^-6) + 2^-14 (relative to ||w||^2), so no
+// candidate that could win is ever skipped.
+//
+// Survivors. Each wave queues its passing (seed, block) pairs in LDS and
+// evaluates them 64 at a time, one per lane, with the exact fp64 evaluation
+// shared with the other engine. Per-block bests live in LDS as 64-bit keys
+// (error bits, seed in the low 24 bits) updated with atomic minimum, so the
+// result does not depend on the order in which survivors are evaluated; ties
+// within 2^-28 relative go to the smaller seed. The first tiles seed every
+// block's best with the exact error of the seed whose bound is smallest in its
+// lane, so that the queue does not fill with hopeless early candidates.
+//
+// Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
+// blocks (128 blocks) and walks all seed tiles once, reusing each A fragment
+// for its 4 block tiles; its B fragments stay in registers for the whole walk.
+#include <cmath>
+
+#include "seedq_exact.h"
+#include "seedq_internal.h"
+
+namespace seedq {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 4;
+constexpr int kNB = 4;               // 32-block tiles per wave
+constexpr int kSlots = kNB * 32;     // blocks per wave
+constexpr int kQCap = 64 + 1024;     // survivor queue entries per wave
+constexpr int kWarmTiles = 2;
+constexpr int kBlocksPerWG = kWaves * kSlots;
+
+struct PairIJ {
+  int i, j;
+};
+__host__ __device__ constexpr PairIJ pair_of(int k) {
+  int i = 0;
+  while (i < kC && k >= kC - i) {
+    k -= kC - i;
+    ++i;
+  }
+  return PairIJ{i, i + k};
+}
+
+struct MfmaArgs {
+  const float* W;
+  int64_t nblocks;
+  const int32_t* list;
+  const int32_t* off;
+  int rung;
+  int K;
+  uint32_t mask;
+  const double* pinv64;
+  const half8* pi16;
+  int64_t ntiles;
+  float one_minus_gamma;
+  uint32_t* seed_out;
+  uint8_t* exp_out;
+  int8_t* q_out;
+  float* err_out;
+};
+
+#define SEEDQ_INLINE __device__ __attribute__((always_inline)) inline
+
+SEEDQ_INLINE void load_block(const float* __restrict__ W, int64_t b, bool ok, float (&w)[kC]) {
+  float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+  if (ok) {
+    const float4* src = reinterpret_cast<const float4*>(W + b * kC);
+    lo = src[0];
+    hi = src[1];
+  }
+  w[0] = lo.x; w[1] = lo.y; w[2] = lo.z; w[3] = lo.w;
+  w[4] = hi.x; w[5] = hi.y; w[6] = hi.z; w[7] = hi.w;
+}
+
+// Exact evaluation of (seed, slot) folded into the slot's key. Out of line:
+// it is off the hot path and keeps the walk's registers free.
+template <int P>
+__device__ __attribute__((noinline)) void eval_into_key(
+    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
+    int64_t b, uint32_t seed, unsigned long long* key) {
+  float w[kC];
+  load_block(W, b, true, w);
+  int e, q[P];
+  const double err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, e, q);
+  atomicMin(key, (unsigned long long)candidate_key(err, seed));
+}
+
+// Evaluates the top min(64, qcount) queue entries, one per lane, until fewer
+// than min_batch remain; returns the new queue count.
+template <int P>
+__device__ __attribute__((noinline)) int flush_queue(
+    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
+    const uint2* queue, const int32_t* blk, unsigned long long* keys, int qcount, int min_batch,
+    int lane) {
+  __threadfence_block();
+  while (qcount >= min_batch && qcount > 0) {
+    const int e = qcount < 64 ? qcount : 64;
+    const int base = qcount - e;
+    if (lane < e) {
+      const uint2 ent = queue[base + lane];
+      if (ent.x != 0u) eval_into_key<P>(W, pinv64, K, mask, blk[ent.y], ent.x, keys + ent.y);
+    }
+    qcount = base;
+  }
+  __threadfence_block();
+  return qcount;
+}
+
+// Final code of one block: the exact evaluation of its winning seed.
+template <int P>
+__device__ __attribute__((noinline)) void write_result(
+    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
+    int64_t b, bool nonzero, unsigned long long key, uint32_t* __restrict__ seed_out,
+    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out, float* __restrict__ err_out) {
+  int q[P];
+  int e = 15;
+  uint32_t seed = 1u;
+  double err = 0.0;
+  if (nonzero) {
+    // every active block has a key after the first tile; seed 1 is a guard
+    seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
+    float w[kC];
+    load_block(W, b, true, w);
+    err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, e, q);
+  } else {
+#pragma unroll
+    for (int p = 0; p < P; ++p) q[p] = 0;  // all-zero block: every seed ties
+  }
+  seed_out[b] = seed;
+  exp_out[b] = uint8_t(e);
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
+    if (p < 4) lo |= byte << (8 * p);
+    else hi |= byte << (8 * (p - 4));
+  }
+  reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
+  if (err_out) err_out[b] = float(err);
+}
+
+SEEDQ_INLINE float fold_max(const floatx16& acc) {
+  float m = fmaxf(fmaxf(acc[0], acc[1]), acc[2]);
+  m = fmaxf(fmaxf(m, acc[3]), acc[4]);
+  m = fmaxf(fmaxf(m, acc[5]), acc[6]);
+  m = fmaxf(fmaxf(m, acc[7]), acc[8]);
+  m = fmaxf(fmaxf(m, acc[9]), acc[10]);
+  m = fmaxf(fmaxf(m, acc[11]), acc[12]);
+  m = fmaxf(fmaxf(m, acc[13]), acc[14]);
+  return fmaxf(m, acc[15]);
+}
+
+SEEDQ_INLINE floatx16 bounds(const half8& a0, const half8& a1, const half8& a2, const half8 (&b)[3]) {
+  floatx16 acc = {};
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0, b[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b[2], acc, 0, 0, 0);
+  return acc;
+}
+
+// Seed of accumulator j of a lane in half h of the wave, for tile seedbase.
+SEEDQ_INLINE uint32_t seed_of(uint32_t seedbase, int j, int h) {
+  return seedbase + 8u * uint32_t(j / 4) + 4u * uint32_t(h) + uint32_t(j % 4);
+}
+
+template <int P>
+__global__ void __launch_bounds__(kWaves * 64)
+search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
+                   const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
+                   const double* __restrict__ pinv64, const half8* __restrict__ pi16,
+                   int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
+                   uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
+                   float* __restrict__ err_out) {
+  __shared__ unsigned long long keys_all[kWaves][kSlots];
+  __shared__ int32_t blk_all[kWaves][kSlots];
+  __shared__ uint2 queue_all[kWaves][kQCap];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n = lane & 31;   // block column of the MFMA tile
+  const int h = lane >> 5;   // which half of the rows / reduction this lane holds
+  unsigned long long* keys = keys_all[wave];
+  int32_t* blk = blk_all[wave];
+  uint2* queue = queue_all[wave];
+
+  int64_t begin = 0, count = nblocks;
+  if (list) {
+    begin = off[rung];
+    count = int64_t(off[rung + 1]) - begin;
+  }
+  const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
+  if (wave_base >= count) return;  // wave-uniform; waves never synchronise
+  const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+  // ---------------------------------------------------------------- prologue
+  half8 bop[kNB][3];
+  float thr[kNB], thr_base[kNB];
+  int ex[kNB];
+  bool active[kNB], valid[kNB];
+#pragma unroll
+  for (int nt = 0; nt < kNB; ++nt) {
+    const int64_t idx = wave_base + nt * 32 + n;
+    valid[nt] = idx < count;
+    const int64_t b = valid[nt] ? (list ? int64_t(list[begin + idx]) : idx) : 0;
+    float w[kC];
+    load_block(W, b, valid[nt], w);
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
+    active[nt] = valid[nt] && amax > 0.f;
+    ex[nt] = active[nt] ? ilogbf(amax) : 0;
+    float ws[kC], ww = 0.f;
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      ws[i] = ldexpf(w[i], -ex[nt]);
+      ww = fmaf(ws[i], ws[i], ww);
+    }
+    // thresholds live in accumulator units (both operands carry 2^12)
+    thr_base[nt] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+    thr[nt] = active[nt] ? -INFINITY : INFINITY;
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k0 = 16 * t + e, k1 = 16 * t + 8 + e;
+        float z0 = 0.f, z1 = 0.f;
+        if (k0 < kPairs) {
+          const PairIJ p = pair_of(k0);
+          z0 = (p.i == p.j ? 1.f : 2.f) * ws[p.i] * ws[p.j] * kOperandScale;
+        }
+        if (k1 < kPairs) {
+          const PairIJ p = pair_of(k1);
+          z1 = (p.i == p.j ? 1.f : 2.f) * ws[p.i] * ws[p.j] * kOperandScale;
+        }
+        bop[nt][t][e] = _Float16(h ? z1 : z0);
+      }
+    }
+    if (h == 0) {
+      keys[nt * 32 + n] = ~0ull;
+      blk[nt * 32 + n] = int32_t(b);
+    }
+  }
+  __threadfence_block();
+
+  // screening thresholds from the current keys
+#define SEEDQ_REFRESH()                                                                    \
+  _Pragma("unroll") for (int nt_ = 0; nt_ < kNB; ++nt_) {                                  \
+    const unsigned long long key_ = keys[nt_ * 32 + n];                                    \
+    if (active[nt_] && key_ != ~0ull) {                                                    \
+      const double bound_ = key_error(key_) * (1.0 + 0x1p-27);                             \
+      thr[nt_] = thr_base[nt_] - __double2float_ru(ldexp(bound_, 24 - 2 * ex[nt_]));       \
+    }                                                                                      \
+  }
+
+  // ---------------------------------------------------------------- warm start
+  // the exact error of each lane's smallest-bound seed of the first tiles
+  const half8* A = pi16;
+  const int64_t nwarm = ntiles < kWarmTiles ? ntiles : kWarmTiles;
+  for (int64_t T = 0; T < nwarm; ++T) {
+    const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
+    const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+      const float m = fold_max(acc);
+      int jb = 15;
+#pragma unroll
+      for (int j = 14; j >= 0; --j)
+        if (acc[j] == m) jb = j;
+      const uint32_t seed = seed_of(seedbase, jb, h);
+      if (active[nt] && seed <= nseeds)
+        eval_into_key<P>(W, pinv64, K, mask, blk[nt * 32 + n], seed, keys + nt * 32 + n);
+    }
+  }
+  __threadfence_block();
+  SEEDQ_REFRESH();
+
+  // ---------------------------------------------------------------- seed walk
+  int qcount = 0;  // wave-uniform
+  half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
+  for (int64_t T = 0; T < ntiles; ++T) {
+    half8 n0 = a0, n1 = a1, n2 = a2;
+    if (T + 1 < ntiles) {
+      const half8* An = A + (T + 1) * 192;
+      n0 = An[lane];
+      n1 = An[64 + lane];
+      n2 = An[128 + lane];
+    }
+    const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+      const float m = fold_max(acc);
+      if (__ballot(m >= thr[nt]) != 0ull) {
+        // queue the passing candidates (fewer than 64 queued on entry, so the
+        // at most 1024 new ones fit)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const bool pass = acc[j] >= thr[nt];
+          const uint64_t mk = __ballot(pass);
+          if (pass) {
+            const uint32_t seed = seed_of(seedbase, j, h);
+            queue[qcount + __popcll(mk & lt)] =
+                make_uint2(seed <= nseeds ? seed : 0u, uint32_t(nt * 32 + n));
+          }
+          qcount += __popcll(mk);
+        }
+        if (qcount >= 64) {
+          qcount = flush_queue<P>(W, pinv64, K, mask, queue, blk, keys, qcount, 64, lane);
+          SEEDQ_REFRESH();
+        }
+      }
+    }
+    a0 = n0;
+    a1 = n1;
+    a2 = n2;
+  }
+  qcount = flush_queue<P>(W, pinv64, K, mask, queue, blk, keys, qcount, 1, lane);
+#undef SEEDQ_REFRESH
+
+  // ---------------------------------------------------------------- results
+#pragma unroll
+  for (int nt = 0; nt < kNB; ++nt) {
+    if (h == 0 && valid[nt])
+      write_result<P>(W, pinv64, K, mask, blk[nt * 32 + n], active[nt], keys[nt * 32 + n],
+                      seed_out, exp_out, q_out, err_out);
+  }
+}
+
+template <int P>
+hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                         const int32_t* d_off, int rung, int K, const void* d_bases,
+                         uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                         hipStream_t stream) {
+  const BasesLayout L = bases_layout(K, P);
+  const char* base = static_cast<const char*>(d_bases);
+  const int64_t blocks = (nblocks + kBlocksPerWG - 1) / kBlocksPerWG;
+  if (blocks == 0) return hipSuccess;
+  MfmaArgs a;
+  a.W = d_W;
+  a.nblocks = nblocks;
+  a.list = d_list;
+  a.off = d_off;
+  a.rung = rung;
+  a.K = K;
+  a.mask = lfsr_mask(K);
+  a.pinv64 = reinterpret_cast<const double*>(base + L.off_pinv64);
+  a.pi16 = reinterpret_cast<const half8*>(base + L.off_pi16);
+  a.ntiles = L.ntiles;
+  const double gamma = std::sqrt(double(P)) * 0x1p-10 * (1.0 + 0x1p-6) + 0x1p-14;
+  a.one_minus_gamma = float(1.0 - gamma);
+  a.seed_out = d_seed;
+  a.exp_out = d_exp;
+  a.q_out = d_q;
+  a.err_out = d_err;
+  hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
+                     a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16, a.ntiles,
+                     a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_search_mfma(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                              const int32_t* d_off, int rung_index, int K, int P,
+                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
+                              float* d_err, hipStream_t stream) {
+  switch (P) {
+#define SEEDQ_CASE(PP)                                                                    \
+  case PP:                                                                                \
+    return launch_mfma_p<PP>(d_W, nblocks, d_list, d_off, rung_index, K, d_bases, d_seed, \
+                             d_exp, d_q, d_err, stream);
+    SEEDQ_CASE(1)
+    SEEDQ_CASE(2)
+    SEEDQ_CASE(3)
+    SEEDQ_CASE(4)
+    SEEDQ_CASE(5)
+    SEEDQ_CASE(6)
+#undef SEEDQ_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace seedq
