@@ -19,14 +19,18 @@
 // shared with the other engine. Per-block bests live in LDS as 64-bit keys
 // (error bits, seed in the low 24 bits) updated with atomic minimum, so the
 // result does not depend on the order in which survivors are evaluated; ties
-// within 2^-28 relative go to the smaller seed. The first tiles seed every
-// block's best with the exact error of the seed whose bound is smallest in its
-// lane, so that the queue does not fill with hopeless early candidates.
+// within 2^-28 relative go to the smaller seed. A pilot pass over the first 64
+// seed tiles (2048 seeds) finds, per lane, the seed with the smallest bound;
+// their exact errors start every block's best, so that the walk meets few
+// hopeless survivors. The final codes go through the same queue.
 //
 // Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
 // blocks (128 blocks) and walks all seed tiles once, reusing each A fragment
 // for its 4 block tiles; its B fragments stay in registers for the whole walk.
+// The bounds of the next block tile are issued to the matrix core before the
+// current one is checked on the vector ALU.
 #include <cmath>
+#include <type_traits>
 
 #include "seedq_exact.h"
 #include "seedq_internal.h"
@@ -40,8 +44,8 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
-constexpr int kQCap = 64 + 1024;     // survivor queue entries per wave
-constexpr int kWarmTiles = 2;
+constexpr int kQCap = 64 + 4 * 1024; // survivor queue entries per wave
+constexpr int kPilotTiles = 64;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
 struct PairIJ {
@@ -87,73 +91,8 @@ SEEDQ_INLINE void load_block(const float* __restrict__ W, int64_t b, bool ok, fl
   w[4] = hi.x; w[5] = hi.y; w[6] = hi.z; w[7] = hi.w;
 }
 
-// Exact evaluation of (seed, slot) folded into the slot's key. Out of line:
-// it is off the hot path and keeps the walk's registers free.
-template <int P>
-__device__ __attribute__((noinline)) void eval_into_key(
-    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
-    int64_t b, uint32_t seed, unsigned long long* key) {
-  float w[kC];
-  load_block(W, b, true, w);
-  int e, q[P];
-  const double err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, e, q);
-  atomicMin(key, (unsigned long long)candidate_key(err, seed));
-}
-
-// Evaluates the top min(64, qcount) queue entries, one per lane, until fewer
-// than min_batch remain; returns the new queue count.
-template <int P>
-__device__ __attribute__((noinline)) int flush_queue(
-    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
-    const uint2* queue, const int32_t* blk, unsigned long long* keys, int qcount, int min_batch,
-    int lane) {
-  __threadfence_block();
-  while (qcount >= min_batch && qcount > 0) {
-    const int e = qcount < 64 ? qcount : 64;
-    const int base = qcount - e;
-    if (lane < e) {
-      const uint2 ent = queue[base + lane];
-      if (ent.x != 0u) eval_into_key<P>(W, pinv64, K, mask, blk[ent.y], ent.x, keys + ent.y);
-    }
-    qcount = base;
-  }
-  __threadfence_block();
-  return qcount;
-}
-
-// Final code of one block: the exact evaluation of its winning seed.
-template <int P>
-__device__ __attribute__((noinline)) void write_result(
-    const float* __restrict__ W, const double* __restrict__ pinv64, int K, uint32_t mask,
-    int64_t b, bool nonzero, unsigned long long key, uint32_t* __restrict__ seed_out,
-    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out, float* __restrict__ err_out) {
-  int q[P];
-  int e = 15;
-  uint32_t seed = 1u;
-  double err = 0.0;
-  if (nonzero) {
-    // every active block has a key after the first tile; seed 1 is a guard
-    seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
-    float w[kC];
-    load_block(W, b, true, w);
-    err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, e, q);
-  } else {
-#pragma unroll
-    for (int p = 0; p < P; ++p) q[p] = 0;  // all-zero block: every seed ties
-  }
-  seed_out[b] = seed;
-  exp_out[b] = uint8_t(e);
-  uint32_t lo = 0, hi = 0;
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
-    if (p < 4) lo |= byte << (8 * p);
-    else hi |= byte << (8 * (p - 4));
-  }
-  reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
-  if (err_out) err_out[b] = float(err);
-}
-
+// Largest of the 16 bounds of a lane (the compiler forms v_max3_f32 and
+// inserts the wait states between the matrix-core write and the reads).
 SEEDQ_INLINE float fold_max(const floatx16& acc) {
   float m = fmaxf(fmaxf(acc[0], acc[1]), acc[2]);
   m = fmaxf(fmaxf(m, acc[3]), acc[4]);
@@ -178,6 +117,15 @@ SEEDQ_INLINE uint32_t seed_of(uint32_t seedbase, int j, int h) {
   return seedbase + 8u * uint32_t(j / 4) + 4u * uint32_t(h) + uint32_t(j % 4);
 }
 
+// Number of lanes below this one whose bit is set in mask.
+SEEDQ_INLINE int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0u));
+}
+
+// Queue entries: seed << 8 | final << 7 | slot (slot < 128). Seed 0 = no-op.
+constexpr uint32_t kFinal = 0x80u;
+static_assert(kSlots <= 128, "slot must fit 7 bits");
+
 template <int P>
 __global__ void __launch_bounds__(kWaves * 64)
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
@@ -188,7 +136,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    float* __restrict__ err_out) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
-  __shared__ uint2 queue_all[kWaves][kQCap];
+  __shared__ uint32_t queue_all[kWaves][kQCap];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -196,7 +144,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
   unsigned long long* keys = keys_all[wave];
   int32_t* blk = blk_all[wave];
-  uint2* queue = queue_all[wave];
+  uint32_t* queue = queue_all[wave];
 
   int64_t begin = 0, count = nblocks;
   if (list) {
@@ -206,7 +154,6 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
   // ---------------------------------------------------------------- prologue
   half8 bop[kNB][3];
@@ -258,41 +205,129 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   }
   __threadfence_block();
 
-  // screening thresholds from the current keys
-#define SEEDQ_REFRESH()                                                                    \
-  _Pragma("unroll") for (int nt_ = 0; nt_ < kNB; ++nt_) {                                  \
-    const unsigned long long key_ = keys[nt_ * 32 + n];                                    \
-    if (active[nt_] && key_ != ~0ull) {                                                    \
-      const double bound_ = key_error(key_) * (1.0 + 0x1p-27);                             \
-      thr[nt_] = thr_base[nt_] - __double2float_ru(ldexp(bound_, 24 - 2 * ex[nt_]));       \
-    }                                                                                      \
-  }
-
-  // ---------------------------------------------------------------- warm start
-  // the exact error of each lane's smallest-bound seed of the first tiles
-  const half8* A = pi16;
-  const int64_t nwarm = ntiles < kWarmTiles ? ntiles : kWarmTiles;
-  for (int64_t T = 0; T < nwarm; ++T) {
-    const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
-    const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+  int qcount = 0;  // wave-uniform
+  // Evaluate the top min(64, qcount) entries, one per lane, until fewer than
+  // min_batch remain; then rebuild the screening thresholds from the keys.
+  auto flush = [&](int min_batch) __attribute__((always_inline)) {
+    __threadfence_block();
+    while (qcount >= min_batch && qcount > 0) {
+      const int e = qcount < 64 ? qcount : 64;
+      const int base = qcount - e;
+      if (lane < e) {
+        const uint32_t ent = queue[base + lane];
+        const uint32_t seed = ent >> 8;
+        const int slot = int(ent & 0x7Fu);
+        if (seed != 0u) {
+          const int64_t b = blk[slot];
+          float w[kC];
+          load_block(W, b, true, w);
+          int qe, q[P];
+          const double err =
+              exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          if (ent & kFinal) {
+            seed_out[b] = seed;
+            exp_out[b] = uint8_t(qe);
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+              const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
+              if (p < 4) lo |= byte << (8 * p);
+              else hi |= byte << (8 * (p - 4));
+            }
+            reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
+            if (err_out) err_out[b] = float(err);
+          } else {
+            atomicMin(&keys[slot], (unsigned long long)candidate_key(err, seed));
+          }
+        }
+      }
+      qcount = base;
+    }
+    __threadfence_block();
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
-      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
-      const float m = fold_max(acc);
-      int jb = 15;
-#pragma unroll
-      for (int j = 14; j >= 0; --j)
-        if (acc[j] == m) jb = j;
-      const uint32_t seed = seed_of(seedbase, jb, h);
-      if (active[nt] && seed <= nseeds)
-        eval_into_key<P>(W, pinv64, K, mask, blk[nt * 32 + n], seed, keys + nt * 32 + n);
+      const unsigned long long key = keys[nt * 32 + n];
+      if (active[nt] && key != ~0ull) {
+        const double bound = key_error(key) * (1.0 + 0x1p-27);
+        thr[nt] = thr_base[nt] - __double2float_ru(ldexp(bound, 24 - 2 * ex[nt]));
+      }
     }
+  };
+
+  const half8* A = pi16;
+
+  // ---------------------------------------------------------------- pilot
+  // Over the first tiles each lane tracks its seed of smallest bound; their
+  // exact errors start every block's best, so that the walk below meets few
+  // hopeless survivors.
+  {
+    const int64_t npilot = ntiles < kPilotTiles ? ntiles : kPilotTiles;
+    float pm[kNB];
+    uint32_t ps[kNB];
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      pm[nt] = -INFINITY;
+      ps[nt] = 0u;
+    }
+    for (int64_t T = 0; T < npilot; ++T) {
+      const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
+      const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+#pragma unroll
+      for (int nt = 0; nt < kNB; ++nt) {
+        const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+        const float m = fold_max(acc);
+        if (m > pm[nt]) {
+          int jb = 15;
+#pragma unroll
+          for (int j = 14; j >= 0; --j)
+            if (acc[j] == m) jb = j;
+          const uint32_t sd = seed_of(seedbase, jb, h);
+          if (sd <= nseeds) {
+            pm[nt] = m;
+            ps[nt] = sd;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const bool put = active[nt] && ps[nt] != 0u;
+      const uint64_t mk = __ballot(put);
+      if (put) queue[qcount + lanes_below(mk)] = (ps[nt] << 8) | uint32_t(nt * 32 + n);
+      qcount += __popcll(mk);
+    }
+    flush(1);
   }
-  __threadfence_block();
-  SEEDQ_REFRESH();
 
   // ---------------------------------------------------------------- seed walk
-  int qcount = 0;  // wave-uniform
+  // Queue the candidates of block tile nt whose bound passes. At most 1024 per
+  // block tile, fewer than 64 are queued at the start of a seed tile, so the
+  // 4 x 1024 of one seed tile always fit.
+  auto check = [&](auto ntc, const floatx16& acc, uint32_t seedbase) __attribute__((always_inline)) {
+    constexpr int nt = decltype(ntc)::value;
+    const float m = fold_max(acc);
+    if (__ballot(m >= thr[nt]) != 0ull) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool pass = acc[j] >= thr[nt];
+        const uint64_t mk = __ballot(pass);
+        if (mk != 0ull) {
+          if (pass) {
+            const uint32_t seed = seed_of(seedbase, j, h);
+            queue[qcount + lanes_below(mk)] =
+                ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
+          }
+          qcount += __popcll(mk);
+        }
+      }
+    }
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  static_assert(kNB == 4, "the walk below unrolls four block tiles");
+
   half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
   for (int64_t T = 0; T < ntiles; ++T) {
     half8 n0 = a0, n1 = a1, n2 = a2;
@@ -303,44 +338,45 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       n2 = An[128 + lane];
     }
     const uint32_t seedbase = uint32_t(T) * 32u + 1u;
-#pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
-      const float m = fold_max(acc);
-      if (__ballot(m >= thr[nt]) != 0ull) {
-        // queue the passing candidates (fewer than 64 queued on entry, so the
-        // at most 1024 new ones fit)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const bool pass = acc[j] >= thr[nt];
-          const uint64_t mk = __ballot(pass);
-          if (pass) {
-            const uint32_t seed = seed_of(seedbase, j, h);
-            queue[qcount + __popcll(mk & lt)] =
-                make_uint2(seed <= nseeds ? seed : 0u, uint32_t(nt * 32 + n));
-          }
-          qcount += __popcll(mk);
-        }
-        if (qcount >= 64) {
-          qcount = flush_queue<P>(W, pinv64, K, mask, queue, blk, keys, qcount, 64, lane);
-          SEEDQ_REFRESH();
-        }
-      }
-    }
+    // the bounds of block tile nt + 1 are issued before block tile nt is checked
+    floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
+    floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
+    check(I0{}, acc0, seedbase);
+    acc0 = bounds(a0, a1, a2, bop[2]);
+    check(I1{}, acc1, seedbase);
+    acc1 = bounds(a0, a1, a2, bop[3]);
+    check(I2{}, acc0, seedbase);
+    check(I3{}, acc1, seedbase);
+    if (qcount >= 64) flush(64);
     a0 = n0;
     a1 = n1;
     a2 = n2;
   }
-  qcount = flush_queue<P>(W, pinv64, K, mask, queue, blk, keys, qcount, 1, lane);
-#undef SEEDQ_REFRESH
+  flush(1);
 
   // ---------------------------------------------------------------- results
+  // the winning seed of every block, evaluated once more to emit its code
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
-    if (h == 0 && valid[nt])
-      write_result<P>(W, pinv64, K, mask, blk[nt * 32 + n], active[nt], keys[nt * 32 + n],
-                      seed_out, exp_out, q_out, err_out);
+    const bool put = h == 0 && active[nt];
+    const uint64_t mk = __ballot(put);
+    if (put) {
+      const unsigned long long key = keys[nt * 32 + n];
+      // every active block has a key after the pilot; seed 1 is a guard
+      const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
+      queue[qcount + lanes_below(mk)] = (seed << 8) | kFinal | uint32_t(nt * 32 + n);
+    }
+    qcount += __popcll(mk);
+    if (h == 0 && valid[nt] && !active[nt]) {
+      // all-zero block: every seed ties, the smallest one wins
+      const int64_t b = blk[nt * 32 + n];
+      seed_out[b] = 1u;
+      exp_out[b] = 15;
+      reinterpret_cast<uint2*>(q_out)[b] = make_uint2(0u, 0u);
+      if (err_out) err_out[b] = 0.f;
+    }
   }
+  flush(1);
 }
 
 template <int P>
