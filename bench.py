@@ -27,19 +27,44 @@ METRIC = "block·seed candidates/sec at K=16, C=8; % MFMA roofline; 1 GPU"
 
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
-PEAK_FP32_VECTOR_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 flop x 2.4 GHz, no packed fp32
-PEAK_FP16_MFMA_TFLOPS = 2500.0
-PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_FP16_MFMA_TFLOPS = 2500.0   # dense fp16 matrix-core peak
+
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+TRAFFIC_FILE = os.path.join(PROFILE_DIR, "search_attn4096_traffic.json")
+KERNEL_SOURCES = ["seedq_search_mfma.hip", "seedq_exact.h", "seedq_internal.h"]
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def search_flops_per_candidate(P: int) -> float:
-    """Algorithmic fp32 operations of the search kernel per (block, seed):
-    the projection c = Q^T w (8P multiply-adds) and its squared norm (P)."""
-    return 2.0 * 8 * P + 2.0 * P
+# The search kernel's dense contraction: for every (block, seed) candidate the
+# least-squares bound w^T Pi_s w over the 36 pair products of the block, i.e.
+# 36 multiply-adds = 72 flops on fp16 matrix cores (the kernel issues the 36
+# padded to 48).
+SEARCH_FLOPS_PER_CANDIDATE = 72.0
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_38477_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per search launch from the committed counter summary, or None
+    when it was taken on another workload or an older kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return float(rec["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(W: np.ndarray, K: int, P: int, target_s: float = 15.0) -> dict:
@@ -111,15 +136,13 @@ def main() -> int:
     d_rob = torch.empty(nb, dtype=torch.uint8, device=dev) if R > 1 else None
     rob_host = torch.empty(nb, dtype=torch.uint8).pin_memory() if R > 1 else None
 
-    ev = {k: torch.cuda.Event(enable_timing=True) for k in
-          ("start", "bases", "search", "decomp")}
-    phase = {"bases": [], "search": [], "decomp": []}
-    cands_holder = {}
+    def events():
+        return {k: torch.cuda.Event(enable_timing=True) for k in ("start", "bases", "search", "decomp")}
 
-    def step(timed: bool):
+    def step(ev):
         rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, rungs, wl.damage, wl.target_bpw, a)
         counts = np.bincount(rob, minlength=R)
-        cands_holder["c"] = int(sum(int(counts[r]) * ((1 << K) - 1) for r, (K, P) in enumerate(rungs)))
+        cands = int(sum(int(counts[r]) * ((1 << K) - 1) for r, (K, P) in enumerate(rungs)))
         ev["start"].record(stream)
         if R > 1:
             rob_host.numpy()[:] = rob
@@ -131,50 +154,43 @@ def main() -> int:
         ev["search"].record(stream)
         sq.seedq_decompress(seed, exp, q, d_rob, rungs, wl.nrows, wl.ncols, 8, W_hat, None, stream)
         ev["decomp"].record(stream)
-        if timed:
-            torch.cuda.synchronize()
-            phase["bases"].append(ev["start"].elapsed_time(ev["bases"]))
-            phase["search"].append(ev["bases"].elapsed_time(ev["search"]))
-            phase["decomp"].append(ev["search"].elapsed_time(ev["decomp"]))
+        return cands
 
     for i in range(args.warmup):
-        step(False)
+        step(events())
         torch.cuda.synchronize()
         log(f"warmup step {i + 1}/{args.warmup} done")
-    # phase timings from a separately synchronised pass of each timed step
+    # timed region: exactly `steps` steps, events recorded on the stream the
+    # kernels run on, read after the closing synchronisation
+    evs = [events() for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(False)
+        cands = step(evs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     log(f"{args.steps} timed steps done in {t1 - t0:.3f} s")
-    for i in range(min(args.steps, 3)):
-        step(True)
+    phase = {"bases": [e["start"].elapsed_time(e["bases"]) for e in evs],
+             "search": [e["bases"].elapsed_time(e["search"]) for e in evs],
+             "decomp": [e["search"].elapsed_time(e["decomp"]) for e in evs]}
     ms = (t1 - t0) * 1000.0 / args.steps
-    cands = cands_holder["c"]
     value = cands / (ms / 1000.0)
 
     search_ms = float(np.mean(phase["search"]))
     decomp_ms = float(np.mean(phase["decomp"]))
     bases_ms = float(np.mean(phase["bases"]))
-    # dominant kernel: the search (one launch per rung)
-    if R == 1:
-        K, P = rungs[0]
-        flops = float(cands) * search_flops_per_candidate(P)
-    else:
-        counts = np.bincount(sq.plan_schedule(wl.nrows, wl.ncols, rungs, wl.damage, wl.target_bpw, a)[0],
-                             minlength=R)
-        flops = float(sum(int(counts[r]) * ((1 << K) - 1) * search_flops_per_candidate(P)
-                          for r, (K, P) in enumerate(rungs)))
+    # dominant kernel: the search (one launch per rung; one launch in total for
+    # a single-rung workload)
+    flops = float(cands) * SEARCH_FLOPS_PER_CANDIDATE
     achieved = flops / (search_ms / 1000.0) / 1e12
-    roofline = {"bound": "alu", "achieved": achieved, "peak": PEAK_FP32_VECTOR_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_VECTOR_TFLOPS, "traffic": None}
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP16_MFMA_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_FP16_MFMA_TFLOPS,
+                "traffic": measured_traffic(wl.name)}
 
     out = {
         "metric": METRIC, "value": value, "unit": "block·seed candidates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
         "config": {"workload": wl.name, "shape": [wl.nrows, wl.ncols], "C": 8,
                    "rungs": [list(r) for r in rungs], "target_bpw": wl.target_bpw,
                    "nblocks": nb, "candidates_per_step": cands, "description": wl.note},

@@ -27,8 +27,10 @@
 // Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
 // blocks (128 blocks) and walks all seed tiles once, reusing each A fragment
 // for its 4 block tiles; its B fragments stay in registers for the whole walk.
-// The bounds of the next block tile are issued to the matrix core before the
-// current one is checked on the vector ALU.
+// Block tiles go to the matrix core in pairs (six products) before the vector
+// ALU folds them, with one branch per pair; the fold waits on its own
+// products, so it is occupancy (several waves per SIMD) that keeps the matrix
+// core busy.
 #include <cmath>
 #include <type_traits>
 
@@ -44,7 +46,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
-constexpr int kQCap = 64 + 4 * 1024; // survivor queue entries per wave
+constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
 constexpr int kPilotTiles = 64;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
@@ -301,12 +303,12 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 
   // ---------------------------------------------------------------- seed walk
   // Queue the candidates of block tile nt whose bound passes. At most 1024 per
-  // block tile, fewer than 64 are queued at the start of a seed tile, so the
-  // 4 x 1024 of one seed tile always fit.
-  auto check = [&](auto ntc, const floatx16& acc, uint32_t seedbase) __attribute__((always_inline)) {
+  // block tile; fewer than 64 are queued before a pair of block tiles, so the
+  // 2 x 1024 of one pair always fit.
+  auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
+                   __attribute__((always_inline)) {
     constexpr int nt = decltype(ntc)::value;
-    const float m = fold_max(acc);
-    if (__ballot(m >= thr[nt]) != 0ull) {
+    if (__ballot(any) != 0ull) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const bool pass = acc[j] >= thr[nt];
@@ -338,16 +340,30 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       n2 = An[128 + lane];
     }
     const uint32_t seedbase = uint32_t(T) * 32u + 1u;
-    // the bounds of block tile nt + 1 are issued before block tile nt is checked
-    floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
-    floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
-    check(I0{}, acc0, seedbase);
-    acc0 = bounds(a0, a1, a2, bop[2]);
-    check(I1{}, acc1, seedbase);
-    acc1 = bounds(a0, a1, a2, bop[3]);
-    check(I2{}, acc0, seedbase);
-    check(I3{}, acc1, seedbase);
-    if (qcount >= 64) flush(64);
+    // two block tiles at a time: six products to the matrix core, then the
+    // folds, one branch per pair
+    {
+      const floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
+      const floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
+      const bool p0 = fold_max(acc0) >= thr[0];
+      const bool p1 = fold_max(acc1) >= thr[1];
+      if (__ballot(p0 | p1) != 0ull) {
+        check(I0{}, acc0, p0, seedbase);
+        check(I1{}, acc1, p1, seedbase);
+        if (qcount >= 64) flush(64);
+      }
+    }
+    {
+      const floatx16 acc2 = bounds(a0, a1, a2, bop[2]);
+      const floatx16 acc3 = bounds(a0, a1, a2, bop[3]);
+      const bool p2 = fold_max(acc2) >= thr[2];
+      const bool p3 = fold_max(acc3) >= thr[3];
+      if (__ballot(p2 | p3) != 0ull) {
+        check(I2{}, acc2, p2, seedbase);
+        check(I3{}, acc3, p3, seedbase);
+        if (qcount >= 64) flush(64);
+      }
+    }
     a0 = n0;
     a1 = n1;
     a2 = n2;
