@@ -173,8 +173,9 @@ class Bases:
 
 
 def plan_schedule(nrows: int, ncols: int, rungs, damage, target_bpw: float, col_importance,
-                  row_importance=None, floor_fraction: float = 0.06):
-    """Rung index per block (numpy uint8 [nblocks]) and the report as a dict."""
+                  row_importance=None, floor_fraction: float = 0.06, out: np.ndarray | None = None):
+    """Rung index per block (numpy uint8 [nblocks], written into ``out`` when
+    given) and the report as a dict."""
     rungs = [tuple(int(v) for v in r) for r in rungs]
     R = len(rungs)
     rung_arr = (Rung * R)(*[Rung(K, P) for K, P in rungs])
@@ -188,7 +189,8 @@ def plan_schedule(nrows: int, ncols: int, rungs, damage, target_bpw: float, col_
                         a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
                         None if rho is None else rho.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
                         float(floor_fraction))
-    out = np.zeros(nrows * (ncols // SEEDQ_BLOCK), dtype=np.uint8)
+    if out is None:
+        out = np.empty(nrows * (ncols // SEEDQ_BLOCK), dtype=np.uint8)
     rep = ScheduleReport()
     seedq_plan_schedule(desc, out, rep)
     report = dict(lam=rep.lambda_, floor_q=rep.floor_q, tie_count=rep.tie_count,

@@ -284,19 +284,38 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
   std::vector<int> cls_tied_from(ncls, -1);
   for (size_t t = 0; t < tied_cls.size(); ++t) cls_tied_from[tied_cls[t]] = tied_from[t];
   int64_t demote_left = T;
-  int64_t check_total = 0;
-  for (int64_t b = 0; b < nb; ++b) {
-    const int c = rho.empty() ? cls_of[b % G] : cls_of[b];
-    int pos = level[c];
-    if (cls_tied_from[c] >= 0 && demote_left > 0) {
-      pos = cls_tied_from[c];
-      --demote_left;
+  if (rho.empty()) {
+    // every row has the same rungs; the first T tied blocks in block order
+    // (row-major) take the lower rung
+    std::vector<uint8_t> row(G);
+    for (int64_t g = 0; g < G; ++g) row[g] = uint8_t(H[level[cls_of[g]]]);
+    for (int64_t r = 0; r < nrows; ++r) std::memcpy(rob + r * G, row.data(), size_t(G));
+    for (int64_t g = 0; g < G; ++g) count[row[g]] += nrows;
+    for (int64_t r = 0; r < nrows && demote_left > 0; ++r)
+      for (int64_t g = 0; g < G && demote_left > 0; ++g) {
+        const int c = cls_of[g];
+        if (cls_tied_from[c] < 0) continue;
+        const int rr = H[cls_tied_from[c]];
+        count[rob[r * G + g]] -= 1;
+        rob[r * G + g] = uint8_t(rr);
+        count[rr] += 1;
+        --demote_left;
+      }
+  } else {
+    for (int64_t b = 0; b < nb; ++b) {
+      const int c = cls_of[b];
+      int pos = level[c];
+      if (cls_tied_from[c] >= 0 && demote_left > 0) {
+        pos = cls_tied_from[c];
+        --demote_left;
+      }
+      const int rr = H[pos];
+      rob[b] = uint8_t(rr);
+      count[rr] += 1;
     }
-    const int rr = H[pos];
-    rob[b] = uint8_t(rr);
-    count[rr] += 1;
-    check_total += int64_t(bits[rr]);
   }
+  int64_t check_total = 0;
+  for (int r = 0; r < R; ++r) check_total += count[r] * int64_t(bits[r]);
   if (rep) {
     std::memset(rep, 0, sizeof(*rep));
     rep->lambda = lam;

@@ -19,10 +19,10 @@
 // shared with the other engine. Per-block bests live in LDS as 64-bit keys
 // (error bits, seed in the low 24 bits) updated with atomic minimum, so the
 // result does not depend on the order in which survivors are evaluated; ties
-// within 2^-28 relative go to the smaller seed. A pilot pass over the first 64
-// seed tiles (2048 seeds) finds, per lane, the seed with the smallest bound;
-// their exact errors start every block's best, so that the walk meets few
-// hopeless survivors. The final codes go through the same queue.
+// within 2^-28 relative go to the smaller seed. A pilot pass over the first
+// seed tile finds, per lane, the seed with the smallest bound; their exact
+// errors start every block's best, so that the walk does not begin with an
+// infinite threshold. The final codes go through the same queue.
 //
 // Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
 // blocks (128 blocks) and walks all seed tiles once, reusing each A fragment
@@ -47,19 +47,65 @@ constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
 constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
-constexpr int kPilotTiles = 64;
+constexpr int kPilotTiles = 1;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
-struct PairIJ {
-  int i, j;
+// Row and column of pair k (i <= j, row-major over the upper triangle) for
+// k < 36; -1 for the padding pairs 36..47. A compile-time table, so that the
+// unrolled prologue indexes it with constants.
+struct PairTable {
+  int i[kPairsPadded];
+  int j[kPairsPadded];
 };
-__host__ __device__ constexpr PairIJ pair_of(int k) {
-  int i = 0;
-  while (i < kC && k >= kC - i) {
-    k -= kC - i;
-    ++i;
+constexpr PairTable make_pair_table() {
+  PairTable t{};
+  int k = 0;
+  for (int i = 0; i < kC; ++i)
+    for (int j = i; j < kC; ++j) {
+      t.i[k] = i;
+      t.j[k] = j;
+      ++k;
+    }
+  for (; k < kPairsPadded; ++k) {
+    t.i[k] = -1;
+    t.j[k] = -1;
   }
-  return PairIJ{i, i + k};
+  return t;
+}
+constexpr PairTable kPairTable = make_pair_table();
+static_assert(kPairTable.i[35] == 7 && kPairTable.j[35] == 7, "36 pairs");
+static_assert(pair_index(2, 5) == 18 && kPairTable.i[18] == 2 && kPairTable.j[18] == 5,
+              "pair numbering agrees with the basis builder");
+
+template <int K0>
+__device__ __forceinline__ float pair_value(const float (&ws)[kC]) {
+  constexpr int i = kPairTable.i[K0], j = kPairTable.j[K0];
+  if constexpr (i < 0) {
+    return 0.f;
+  } else {
+    return (i == j ? 1.f : 2.f) * ws[i] * ws[j] * kOperandScale;
+  }
+}
+
+template <int T, int E>
+__device__ __forceinline__ _Float16 b_element(const float (&ws)[kC], int h) {
+  const float z0 = pair_value<16 * T + E>(ws);
+  const float z1 = pair_value<16 * T + 8 + E>(ws);
+  return _Float16(h ? z1 : z0);
+}
+
+template <int T>
+__device__ __forceinline__ half8 b_fragment(const float (&ws)[kC], int h) {
+  half8 v;
+  v[0] = b_element<T, 0>(ws, h);
+  v[1] = b_element<T, 1>(ws, h);
+  v[2] = b_element<T, 2>(ws, h);
+  v[3] = b_element<T, 3>(ws, h);
+  v[4] = b_element<T, 4>(ws, h);
+  v[5] = b_element<T, 5>(ws, h);
+  v[6] = b_element<T, 6>(ws, h);
+  v[7] = b_element<T, 7>(ws, h);
+  return v;
 }
 
 struct MfmaArgs {
@@ -183,23 +229,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     // thresholds live in accumulator units (both operands carry 2^12)
     thr_base[nt] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
     thr[nt] = active[nt] ? -INFINITY : INFINITY;
-#pragma unroll
-    for (int t = 0; t < 3; ++t) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int k0 = 16 * t + e, k1 = 16 * t + 8 + e;
-        float z0 = 0.f, z1 = 0.f;
-        if (k0 < kPairs) {
-          const PairIJ p = pair_of(k0);
-          z0 = (p.i == p.j ? 1.f : 2.f) * ws[p.i] * ws[p.j] * kOperandScale;
-        }
-        if (k1 < kPairs) {
-          const PairIJ p = pair_of(k1);
-          z1 = (p.i == p.j ? 1.f : 2.f) * ws[p.i] * ws[p.j] * kOperandScale;
-        }
-        bop[nt][t][e] = _Float16(h ? z1 : z0);
-      }
-    }
+    bop[nt][0] = b_fragment<0>(ws, h);
+    bop[nt][1] = b_fragment<1>(ws, h);
+    bop[nt][2] = b_fragment<2>(ws, h);
     if (h == 0) {
       keys[nt * 32 + n] = ~0ull;
       blk[nt * 32 + n] = int32_t(b);
@@ -259,9 +291,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const half8* A = pi16;
 
   // ---------------------------------------------------------------- pilot
-  // Over the first tiles each lane tracks its seed of smallest bound; their
-  // exact errors start every block's best, so that the walk below meets few
-  // hopeless survivors.
+  // Over the first tile(s) each lane tracks its seed of smallest bound; their
+  // exact errors start every block's best. (Longer pilots cost more matrix
+  // time than the survivors they save.)
   {
     const int64_t npilot = ntiles < kPilotTiles ? ntiles : kPilotTiles;
     float pm[kNB];
