@@ -284,3 +284,31 @@ def test_seed_bit_flip_footprint(sq, torch):
     diff = (clean != dirty).cpu().numpy().reshape(-1, 8)
     assert np.nonzero(diff.any(axis=1))[0].tolist() == [333]
     assert diff.sum() <= 8
+
+
+def test_search_full_size_three_rungs_sampled(sq, oq, torch):
+    # 4096 x 11008 at 3.5 bits per weight over (12,2)/(16,3)/(20,4), with the
+    # schedule, compaction and one search launch per rung exactly as the
+    # benchmark runs them; the oracle checks evenly spaced blocks of every rung
+    wl = synthetic.WORKLOADS["reduced"]
+    W = synthetic.workload_weights(wl)
+    a = synthetic.importance_profile(wl.ncols)
+    rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
+    assert rep["total_bits"] == rep["budget_bits"]
+    bases = [sq.build_bases(K, P) for K, P in wl.rungs]
+    seed, e, q, err = sq.compress(_dev(torch, W), bases, rung_of_block=_dev(torch, rob))
+    W_hat, _ = sq.decompress(seed, e, q, wl.rungs, wl.nrows, wl.ncols, rung_of_block=_dev(torch, rob))
+    torch.cuda.synchronize()
+    seed, e, q, err = seed.cpu().numpy().view(np.uint32), e.cpu().numpy(), q.cpu().numpy(), err.cpu().numpy()
+    blocks = W.reshape(-1, 8).astype(np.float64)
+    d = blocks - W_hat.cpu().numpy().reshape(-1, 8).astype(np.float64)
+    direct = (d * d).sum(axis=1)
+    assert np.all(np.abs(direct - err) <= 1e-5 * direct + 1e-30)
+    for r, (K, P) in enumerate(wl.rungs):
+        sel = np.nonzero(rob == r)[0]
+        assert np.all((seed[sel] >= 1) & (seed[sel] < (1 << K)))
+        assert not q[sel][:, P:].any()
+        n = 12 if K == 20 else 48
+        idx = sel[np.linspace(0, len(sel) - 1, n).astype(np.int64)]
+        check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx],
+                     f"reduced rung{r}")
