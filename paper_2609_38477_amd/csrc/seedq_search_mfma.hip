@@ -47,7 +47,6 @@ constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
 constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
-constexpr int kPilotTiles = 1;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
 // Row and column of pair k (i <= j, row-major over the upper triangle) for
@@ -139,18 +138,20 @@ SEEDQ_INLINE void load_block(const float* __restrict__ W, int64_t b, bool ok, fl
   w[4] = hi.x; w[5] = hi.y; w[6] = hi.z; w[7] = hi.w;
 }
 
-// Largest of the 16 bounds of a lane (the compiler forms v_max3_f32 and
-// inserts the wait states between the matrix-core write and the reads).
+// Largest of the 16 bounds of a lane. The bounds are finite (products of
+// finite fp16 values), so the NaN-propagating maximum equals the IEEE maxNum
+// here; it needs no operand canonicalisation and folds as v_maximum3_f32. The
+// compiler inserts the wait states between the matrix-core write and the reads.
 SEEDQ_INLINE float fold_max(const floatx16& acc) {
-  float m = fmaxf(fmaxf(acc[0], acc[1]), acc[2]);
-  m = fmaxf(fmaxf(m, acc[3]), acc[4]);
-  m = fmaxf(fmaxf(m, acc[5]), acc[6]);
-  m = fmaxf(fmaxf(m, acc[7]), acc[8]);
-  m = fmaxf(fmaxf(m, acc[9]), acc[10]);
-  m = fmaxf(fmaxf(m, acc[11]), acc[12]);
-  m = fmaxf(fmaxf(m, acc[13]), acc[14]);
-  return fmaxf(m, acc[15]);
+  float m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(acc[0], acc[1]), acc[2]);
+#pragma unroll
+  for (int j = 3; j < 15; j += 2)
+    m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, acc[j]), acc[j + 1]);
+  return __builtin_elementwise_maximum(m, acc[15]);
 }
+
+// Wave-wide vote (a bit per lane whose p is set).
+SEEDQ_INLINE uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
 SEEDQ_INLINE floatx16 bounds(const half8& a0, const half8& a1, const half8& a2, const half8 (&b)[3]) {
   floatx16 acc = {};
@@ -204,34 +205,10 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
 
   // ---------------------------------------------------------------- prologue
-  half8 bop[kNB][3];
-  float thr[kNB], thr_base[kNB];
-  int ex[kNB];
-  bool active[kNB], valid[kNB];
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
     const int64_t idx = wave_base + nt * 32 + n;
-    valid[nt] = idx < count;
-    const int64_t b = valid[nt] ? (list ? int64_t(list[begin + idx]) : idx) : 0;
-    float w[kC];
-    load_block(W, b, valid[nt], w);
-    float amax = 0.f;
-#pragma unroll
-    for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
-    active[nt] = valid[nt] && amax > 0.f;
-    ex[nt] = active[nt] ? ilogbf(amax) : 0;
-    float ws[kC], ww = 0.f;
-#pragma unroll
-    for (int i = 0; i < kC; ++i) {
-      ws[i] = ldexpf(w[i], -ex[nt]);
-      ww = fmaf(ws[i], ws[i], ww);
-    }
-    // thresholds live in accumulator units (both operands carry 2^12)
-    thr_base[nt] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
-    thr[nt] = active[nt] ? -INFINITY : INFINITY;
-    bop[nt][0] = b_fragment<0>(ws, h);
-    bop[nt][1] = b_fragment<1>(ws, h);
-    bop[nt][2] = b_fragment<2>(ws, h);
+    const int64_t b = idx < count ? (list ? int64_t(list[begin + idx]) : idx) : 0;
     if (h == 0) {
       keys[nt * 32 + n] = ~0ull;
       blk[nt * 32 + n] = int32_t(b);
@@ -239,9 +216,45 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   }
   __threadfence_block();
 
+  // Per-lane block data: the B fragments (2^12-scaled pair products of the
+  // block scaled by a power of two so that max |w_i| lies in [1, 2)) and the
+  // screening threshold in accumulator units. Rebuilt from W and the keys after
+  // every exact evaluation, so that none of it is live across that code.
+  half8 bop[kNB][3];
+  float thr[kNB];
+  auto setup = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const bool valid = wave_base + nt * 32 + n < count;
+      float w[kC];
+      load_block(W, blk[nt * 32 + n], valid, w);
+      float amax = 0.f;
+#pragma unroll
+      for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
+      const bool active = valid && amax > 0.f;
+      const int ex = active ? ilogbf(amax) : 0;
+      float ws[kC], ww = 0.f;
+#pragma unroll
+      for (int i = 0; i < kC; ++i) {
+        ws[i] = ldexpf(w[i], -ex);
+        ww = fmaf(ws[i], ws[i], ww);
+      }
+      bop[nt][0] = b_fragment<0>(ws, h);
+      bop[nt][1] = b_fragment<1>(ws, h);
+      bop[nt][2] = b_fragment<2>(ws, h);
+      // -inf before a block's first exact error, +inf for blocks not searched
+      const unsigned long long key = keys[nt * 32 + n];
+      const float thr_base = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+      const double bound = key_error(key) * (1.0 + 0x1p-27);
+      thr[nt] = !active ? INFINITY
+                : key == ~0ull ? -INFINITY
+                : thr_base - __double2float_ru(ldexp(bound, 24 - 2 * ex));
+    }
+  };
+
   int qcount = 0;  // wave-uniform
   // Evaluate the top min(64, qcount) entries, one per lane, until fewer than
-  // min_batch remain; then rebuild the screening thresholds from the keys.
+  // min_batch remain; then rebuild the block data and thresholds.
   auto flush = [&](int min_batch) __attribute__((always_inline)) {
     __threadfence_block();
     while (qcount >= min_batch && qcount > 0) {
@@ -278,56 +291,31 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       qcount = base;
     }
     __threadfence_block();
-#pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const unsigned long long key = keys[nt * 32 + n];
-      if (active[nt] && key != ~0ull) {
-        const double bound = key_error(key) * (1.0 + 0x1p-27);
-        thr[nt] = thr_base[nt] - __double2float_ru(ldexp(bound, 24 - 2 * ex[nt]));
-      }
-    }
+    setup();
   };
 
   const half8* A = pi16;
+  setup();
 
   // ---------------------------------------------------------------- pilot
-  // Over the first tile(s) each lane tracks its seed of smallest bound; their
-  // exact errors start every block's best. (Longer pilots cost more matrix
-  // time than the survivors they save.)
+  // Over the first tile each lane takes its seed of smallest bound; their exact
+  // errors start every block's best. (Longer pilots cost more matrix time than
+  // the survivors they save.)
   {
-    const int64_t npilot = ntiles < kPilotTiles ? ntiles : kPilotTiles;
-    float pm[kNB];
-    uint32_t ps[kNB];
+    const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
-      pm[nt] = -INFINITY;
-      ps[nt] = 0u;
-    }
-    for (int64_t T = 0; T < npilot; ++T) {
-      const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
-      const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+      const float m = fold_max(acc);
+      int jb = 15;
 #pragma unroll
-      for (int nt = 0; nt < kNB; ++nt) {
-        const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
-        const float m = fold_max(acc);
-        if (m > pm[nt]) {
-          int jb = 15;
-#pragma unroll
-          for (int j = 14; j >= 0; --j)
-            if (acc[j] == m) jb = j;
-          const uint32_t sd = seed_of(seedbase, jb, h);
-          if (sd <= nseeds) {
-            pm[nt] = m;
-            ps[nt] = sd;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const bool put = active[nt] && ps[nt] != 0u;
-      const uint64_t mk = __ballot(put);
-      if (put) queue[qcount + lanes_below(mk)] = (ps[nt] << 8) | uint32_t(nt * 32 + n);
+      for (int j = 14; j >= 0; --j)
+        if (acc[j] == m) jb = j;
+      // seeds 1..32 all exist (K >= 8)
+      const uint32_t sd = seed_of(1u, jb, h);
+      const bool put = thr[nt] != INFINITY;
+      const uint64_t mk = ballot(put);
+      if (put) queue[qcount + lanes_below(mk)] = (sd << 8) | uint32_t(nt * 32 + n);
       qcount += __popcll(mk);
     }
     flush(1);
@@ -340,11 +328,11 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
                    __attribute__((always_inline)) {
     constexpr int nt = decltype(ntc)::value;
-    if (__ballot(any) != 0ull) {
+    if (ballot(any) != 0ull) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const bool pass = acc[j] >= thr[nt];
-        const uint64_t mk = __ballot(pass);
+        const uint64_t mk = ballot(pass);
         if (mk != 0ull) {
           if (pass) {
             const uint32_t seed = seed_of(seedbase, j, h);
@@ -362,61 +350,80 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   using I3 = std::integral_constant<int, 3>;
   static_assert(kNB == 4, "the walk below unrolls four block tiles");
 
-  half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
-  for (int64_t T = 0; T < ntiles; ++T) {
-    half8 n0 = a0, n1 = a1, n2 = a2;
-    if (T + 1 < ntiles) {
-      const half8* An = A + (T + 1) * 192;
-      n0 = An[lane];
-      n1 = An[64 + lane];
-      n2 = An[128 + lane];
-    }
+  // Seed-tile fragments; the index is clamped to the last tile so that every
+  // load is unconditional and each wait covers only the tile it is for.
+  const int64_t last = ntiles - 1;
+  auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
+    const half8* At = A + (T < last ? T : last) * 192;
+    f[0] = At[lane];
+    f[1] = At[64 + lane];
+    f[2] = At[128 + lane];
+  };
+
+  // Seed tile T (fragments c) against the four block tiles, two block tiles
+  // at a time: six products to the matrix core, then the folds, one branch per
+  // pair. An exact evaluation rebuilds the block data and reloads both this
+  // tile's fragments and those of the other set (tile To, in o).
+  auto tile = [&](half8 (&c)[3], int64_t T, half8 (&o)[3], int64_t To)
+                  __attribute__((always_inline)) {
     const uint32_t seedbase = uint32_t(T) * 32u + 1u;
-    // two block tiles at a time: six products to the matrix core, then the
-    // folds, one branch per pair
     {
-      const floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
-      const floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
+      const floatx16 acc0 = bounds(c[0], c[1], c[2], bop[0]);
+      const floatx16 acc1 = bounds(c[0], c[1], c[2], bop[1]);
       const bool p0 = fold_max(acc0) >= thr[0];
       const bool p1 = fold_max(acc1) >= thr[1];
-      if (__ballot(p0 | p1) != 0ull) {
+      if ((ballot(p0) | ballot(p1)) != 0ull) {
         check(I0{}, acc0, p0, seedbase);
         check(I1{}, acc1, p1, seedbase);
-        if (qcount >= 64) flush(64);
+        if (qcount >= 64) {
+          flush(64);
+          load_tile(T, c);
+          load_tile(To, o);
+        }
       }
     }
     {
-      const floatx16 acc2 = bounds(a0, a1, a2, bop[2]);
-      const floatx16 acc3 = bounds(a0, a1, a2, bop[3]);
+      const floatx16 acc2 = bounds(c[0], c[1], c[2], bop[2]);
+      const floatx16 acc3 = bounds(c[0], c[1], c[2], bop[3]);
       const bool p2 = fold_max(acc2) >= thr[2];
       const bool p3 = fold_max(acc3) >= thr[3];
-      if (__ballot(p2 | p3) != 0ull) {
+      if ((ballot(p2) | ballot(p3)) != 0ull) {
         check(I2{}, acc2, p2, seedbase);
         check(I3{}, acc3, p3, seedbase);
-        if (qcount >= 64) flush(64);
+        if (qcount >= 64) {
+          flush(64);
+          load_tile(To, o);
+        }
       }
     }
-    a0 = n0;
-    a1 = n1;
-    a2 = n2;
+  };
+
+  // Two fragment sets in turn: one tile is loaded while the other is screened.
+  half8 x[3], y[3];
+  load_tile(0, x);
+  for (int64_t T = 0; T < ntiles; T += 2) {
+    load_tile(T + 1, y);
+    tile(x, T, y, T + 1);
+    load_tile(T + 2, x);
+    if (T + 1 < ntiles) tile(y, T + 1, x, T + 2);
   }
   flush(1);
 
   // ---------------------------------------------------------------- results
-  // the winning seed of every block, evaluated once more to emit its code
+  // The winning seed of every block, evaluated once more to emit its code.
+  // Every searched block holds a key after the pilot; a valid block without
+  // one is all zero, where every seed ties and the smallest wins.
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
-    const bool put = h == 0 && active[nt];
-    const uint64_t mk = __ballot(put);
-    if (put) {
-      const unsigned long long key = keys[nt * 32 + n];
-      // every active block has a key after the pilot; seed 1 is a guard
-      const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
-      queue[qcount + lanes_below(mk)] = (seed << 8) | kFinal | uint32_t(nt * 32 + n);
-    }
+    const bool valid = wave_base + nt * 32 + n < count;
+    const unsigned long long key = keys[nt * 32 + n];
+    const bool put = h == 0 && valid && key != ~0ull;
+    const uint64_t mk = ballot(put);
+    if (put)
+      queue[qcount + lanes_below(mk)] =
+          (uint32_t(key & 0xFFFFFFull) << 8) | kFinal | uint32_t(nt * 32 + n);
     qcount += __popcll(mk);
-    if (h == 0 && valid[nt] && !active[nt]) {
-      // all-zero block: every seed ties, the smallest one wins
+    if (h == 0 && valid && key == ~0ull) {
       const int64_t b = blk[nt * 32 + n];
       seed_out[b] = 1u;
       exp_out[b] = 15;
