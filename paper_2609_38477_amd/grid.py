@@ -1,0 +1,156 @@
+"""Uniform builds over a grid of rungs and the per-block error ratios across rungs.
+
+The encoder's dominant cost is one exhaustive seed search per rung of the grid
+S in {8..16}, k in {2..6} (appendix on cost; appendix "Rung grids", Table
+grids): every uniform build is a SeedLM compression of the same blocks at
+another rung. The appendix on per-block error across rungs (Table rungshape)
+then divides each block's reconstruction error at rung g by the same block's
+error at (16, 3) and summarises the ratios by their median, 10 % and 90 %
+quantiles and the standard deviation of their logarithm.
+
+``build_grid`` runs those uniform builds through the library (one basis stack
+and one ``seedq_compress`` call per rung, all on the GPU); ``rungshape``
+computes the ratio summary from the per-block errors on the host.
+
+    python -m paper_2609_38477_amd.grid [--workload attn4096] [--rungs paper|rungshape]
+
+prints one JSON line with the per-rung timings and the ratio table.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+import time
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import (SEEDQ_BLOCK, seedq_bases_bytes, seedq_build_bases, seedq_compress,
+               seedq_compress_workspace_bytes, Bases)
+
+# The grid the paper builds rungs from (section 3.1: S in {8..16}, k in {2..6}).
+PAPER_GRID = tuple((S, k) for S in range(8, 17) for k in range(2, 7))
+# The rungs of Table rungshape and its reference rung.
+RUNGSHAPE_RUNGS = ((10, 3), (12, 3), (14, 3), (14, 4), (16, 5))
+REFERENCE_RUNG = (16, 3)
+
+
+def rate_bpw(K: int, P: int) -> float:
+    """Bits per weight of rung (K, P): (K + 4P + 4) / 8 (eq. (rate), m = e = 4)."""
+    return (K + 4 * P + 4) / SEEDQ_BLOCK
+
+
+@dataclass
+class GridResult:
+    rungs: tuple
+    err: dict                      # rung -> torch fp32 [nblocks] on the device
+    search_ms: dict = field(default_factory=dict)   # rung -> search kernel time (HIP events)
+    bases_ms: dict = field(default_factory=dict)    # rung -> basis build time (HIP events)
+    nblocks: int = 0
+
+    def candidates(self, rung) -> int:
+        return self.nblocks * ((1 << rung[0]) - 1)
+
+
+def build_grid(W, rungs=PAPER_GRID, stream=None) -> GridResult:
+    """Uniform compression of every block of W (torch fp32 [nrows, ncols] on the
+    GPU) at each rung; returns the exact per-block errors and the per-rung GPU
+    times (HIP events on the stream the kernels run on)."""
+    import torch
+    nrows, ncols = W.shape
+    nb = nrows * ncols // SEEDQ_BLOCK
+    dev = W.device
+    stream = stream or torch.cuda.current_stream(dev)
+    seed = torch.empty(nb, dtype=torch.int32, device=dev)
+    exp = torch.empty(nb, dtype=torch.uint8, device=dev)
+    q = torch.empty((nb, 8), dtype=torch.int8, device=dev)
+    assert seedq_compress_workspace_bytes(nrows, ncols, SEEDQ_BLOCK, 1) == 0
+    res = GridResult(tuple(tuple(r) for r in rungs), {}, nblocks=nb)
+    marks = []
+    for K, P in res.rungs:
+        buf = torch.empty(seedq_bases_bytes(K, P), dtype=torch.uint8, device=dev)
+        err = torch.empty(nb, dtype=torch.float32, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        seedq_build_bases(K, P, SEEDQ_BLOCK, buf, None, None, stream)
+        ev[1].record(stream)
+        seedq_compress(W, nrows, ncols, SEEDQ_BLOCK, None, [Bases(K, P, buf)], seed, exp, q, err,
+                       None, 0, stream)
+        ev[2].record(stream)
+        res.err[(K, P)] = err
+        marks.append(((K, P), ev, buf))
+    stream.synchronize()
+    for rung, ev, _ in marks:
+        res.bases_ms[rung] = ev[0].elapsed_time(ev[1])
+        res.search_ms[rung] = ev[1].elapsed_time(ev[2])
+    return res
+
+
+def rungshape(err: dict, rungs=RUNGSHAPE_RUNGS, ref=REFERENCE_RUNG) -> list:
+    """Per-block error ratio err_g / err_ref over the blocks where both errors are
+    positive (a ratio of a zero error is undefined), summarised per rung as the
+    median, the 10 % and 90 % quantiles (numpy's linear interpolation) and the
+    population standard deviation of the natural log of the ratio (appendix on
+    per-block error across rungs, Table rungshape). ``err`` maps rung -> numpy
+    or torch array of per-block errors."""
+    def host(a):
+        return np.asarray(a.detach().cpu().numpy() if hasattr(a, "detach") else a, dtype=np.float64)
+    e0 = host(err[tuple(ref)])
+    rows = []
+    for rung in rungs:
+        e = host(err[tuple(rung)])
+        keep = (e0 > 0) & (e > 0) & np.isfinite(e0) & np.isfinite(e)
+        r = e[keep] / e0[keep]
+        rows.append({"rung": list(rung), "rate_bpw": rate_bpw(*rung), "blocks": int(keep.sum()),
+                     "median": float(np.median(r)), "q10": float(np.quantile(r, 0.10)),
+                     "q90": float(np.quantile(r, 0.90)), "sd_log": float(np.std(np.log(r)))})
+    return rows
+
+
+def mean_errors(err: dict) -> dict:
+    """Mean per-block error of every rung: a weight-space stand-in for the
+    damage e(g) of a uniform build (no data is read)."""
+    return {tuple(r): float(np.mean(np.asarray(e.detach().cpu().numpy(), dtype=np.float64)))
+            for r, e in err.items()}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", default="attn4096")
+    ap.add_argument("--rungs", choices=("paper", "rungshape"), default="paper")
+    args = ap.parse_args(argv)
+    import torch
+    import os
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    import synthetic
+    if not torch.cuda.is_available():
+        print("the grid build needs a GPU", file=sys.stderr)
+        return 2
+    wl = synthetic.WORKLOADS[args.workload]
+    W = torch.from_numpy(synthetic.workload_weights(wl)).cuda()
+    rungs = PAPER_GRID if args.rungs == "paper" else tuple(sorted(set(RUNGSHAPE_RUNGS) | {REFERENCE_RUNG}))
+    build_grid(W, rungs=((8, 2),))  # warm-up: module load and first launch
+    t0 = time.perf_counter()
+    res = build_grid(W, rungs=rungs)
+    wall = time.perf_counter() - t0
+    table = rungshape(res.err)
+    me = mean_errors(res.err)
+    per_rung = [{"rung": list(r), "rate_bpw": rate_bpw(*r), "search_ms": res.search_ms[r],
+                 "bases_ms": res.bases_ms[r],
+                 "candidates_per_s": res.candidates(r) / (res.search_ms[r] / 1e3),
+                 "mean_err": me[r]} for r in res.rungs]
+    total_c = sum(res.candidates(r) for r in res.rungs)
+    total_ms = sum(res.search_ms.values())
+    print(json.dumps({"workload": wl.name, "shape": [wl.nrows, wl.ncols], "nblocks": res.nblocks,
+                      "rungs": len(res.rungs), "wall_s": wall, "search_ms_total": total_ms,
+                      "candidates_total": total_c,
+                      "candidates_per_s": total_c / (total_ms / 1e3),
+                      "rungshape": table, "per_rung": per_rung}), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
