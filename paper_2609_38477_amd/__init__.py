@@ -75,6 +75,9 @@ def lib() -> ctypes.CDLL:
         L.seedq_plan_schedule.restype = ctypes.c_int
         L.seedq_plan_schedule.argtypes = [ctypes.POINTER(ScheduleDesc), vp,
                                           ctypes.POINTER(ScheduleReport)]
+        L.seedq_derive_schedule.restype = ctypes.c_int
+        L.seedq_derive_schedule.argtypes = [ctypes.POINTER(ScheduleDesc), ctypes.c_double,
+                                            ctypes.c_double, i64, vp]
         L.seedq_bases_bytes.restype = ctypes.c_int
         L.seedq_bases_bytes.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
         L.seedq_build_bases.restype = ctypes.c_int
@@ -126,6 +129,14 @@ def seedq_plan_schedule(desc: ScheduleDesc, rung_of_block: np.ndarray,
     _check(rc, "seedq_plan_schedule")
 
 
+def seedq_derive_schedule(desc: ScheduleDesc, lam: float, floor_q: float, tie_count: int,
+                          rung_of_block: np.ndarray) -> None:
+    assert rung_of_block.dtype == np.uint8 and rung_of_block.flags.c_contiguous
+    rc = lib().seedq_derive_schedule(ctypes.byref(desc), float(lam), float(floor_q),
+                                     int(tie_count), rung_of_block.ctypes.data)
+    _check(rc, "seedq_derive_schedule")
+
+
 def seedq_bases_bytes(K: int, P: int, C: int = SEEDQ_BLOCK) -> int:
     out = ctypes.c_size_t(0)
     _check(lib().seedq_bases_bytes(K, P, C, ctypes.byref(out)), "seedq_bases_bytes")
@@ -172,23 +183,44 @@ class Bases:
     pinv: object = None       # fp32 [P, 2^K-1, 8] or None
 
 
+def _schedule_desc(nrows, ncols, rungs, damage, target_bpw, col_importance, row_importance,
+                   floor_fraction):
+    """A ScheduleDesc and the arrays it points into (keep them alive while it is used)."""
+    rungs = [tuple(int(v) for v in r) for r in rungs]
+    R = len(rungs)
+    rung_arr = (Rung * R)(*[Rung(K, P) for K, P in rungs])
+    dmg_np = None if damage is None else np.ascontiguousarray(damage, dtype=np.float64)
+    a = np.ascontiguousarray(col_importance, dtype=np.float32)
+    rho = None if row_importance is None else np.ascontiguousarray(row_importance, dtype=np.float32)
+    desc = ScheduleDesc(nrows, ncols, SEEDQ_BLOCK, R, rung_arr,
+                        None if dmg_np is None else dmg_np.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                        float(target_bpw), a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                        None if rho is None else rho.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                        float(floor_fraction))
+    return desc, (rung_arr, dmg_np, a, rho)
+
+
+def derive_schedule(nrows: int, ncols: int, rungs, damage, col_importance, lam: float,
+                    floor_q: float, tie_count: int, row_importance=None,
+                    out: np.ndarray | None = None) -> np.ndarray:
+    """Decoder-side rung index per block from the stored lambda, floor value and
+    tie count (numpy uint8 [nblocks])."""
+    desc, keep = _schedule_desc(nrows, ncols, rungs, damage, 0.0, col_importance, row_importance,
+                                0.0)
+    if out is None:
+        out = np.empty(nrows * (ncols // SEEDQ_BLOCK), dtype=np.uint8)
+    seedq_derive_schedule(desc, lam, floor_q, tie_count, out)
+    del keep
+    return out
+
+
 def plan_schedule(nrows: int, ncols: int, rungs, damage, target_bpw: float, col_importance,
                   row_importance=None, floor_fraction: float = 0.06, out: np.ndarray | None = None):
     """Rung index per block (numpy uint8 [nblocks], written into ``out`` when
     given) and the report as a dict."""
-    rungs = [tuple(int(v) for v in r) for r in rungs]
     R = len(rungs)
-    rung_arr = (Rung * R)(*[Rung(K, P) for K, P in rungs])
-    dmg = None
-    if damage is not None:
-        dmg_np = np.ascontiguousarray(damage, dtype=np.float64)
-        dmg = dmg_np.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
-    a = np.ascontiguousarray(col_importance, dtype=np.float32)
-    rho = None if row_importance is None else np.ascontiguousarray(row_importance, dtype=np.float32)
-    desc = ScheduleDesc(nrows, ncols, SEEDQ_BLOCK, R, rung_arr, dmg, float(target_bpw),
-                        a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
-                        None if rho is None else rho.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
-                        float(floor_fraction))
+    desc, keep = _schedule_desc(nrows, ncols, rungs, damage, target_bpw, col_importance,
+                                row_importance, floor_fraction)
     if out is None:
         out = np.empty(nrows * (ncols // SEEDQ_BLOCK), dtype=np.uint8)
     rep = ScheduleReport()

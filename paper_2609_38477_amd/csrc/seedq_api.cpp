@@ -35,6 +35,11 @@ int seedq_plan_schedule(const seedq_schedule_desc* desc, uint8_t* rung_of_block,
   return plan_schedule(desc, rung_of_block, report);
 }
 
+int seedq_derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,
+                          int64_t tie_count, uint8_t* rung_of_block) {
+  return derive_schedule(desc, lambda, floor_q, tie_count, rung_of_block);
+}
+
 int seedq_bases_bytes(int32_t K, int32_t P, int32_t C, size_t* bytes) {
   if (!bytes) return SEEDQ_EINVAL;
   if (C != kC || !rung_supported(K, P)) return SEEDQ_EUNSUPPORTED;

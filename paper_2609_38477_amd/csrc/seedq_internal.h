@@ -125,6 +125,8 @@ hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const
                              float* d_W_hat, int32_t* d_acc, hipStream_t stream);
 
 // Host planner (seedq_schedule.cpp).
+int derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,
+                    int64_t tie_count, uint8_t* rung_of_block);
 int plan_schedule(const seedq_schedule_desc* desc, uint8_t* rung_of_block,
                   seedq_schedule_report* report);
 

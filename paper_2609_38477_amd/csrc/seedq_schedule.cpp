@@ -45,10 +45,21 @@ double breakpoint(double v, double s) {
   return lam;
 }
 
-}  // namespace
+// What the encoder and the decoder both derive from the descriptor: block
+// importance factors (unit mean, fixed evaluation order), the hull and its
+// slopes. Returns SEEDQ_OK or the error code of the first problem found.
+struct Prepared {
+  int64_t nrows = 0, G = 0, nb = 0;
+  std::vector<double> bits;   // K + 4P + 4 per rung
+  std::vector<double> abar;   // per column group, unit mean
+  std::vector<double> rho;    // per row, unit mean; empty for rho = 1
+  std::vector<int> H;         // hull vertices (rung indices), increasing rate
+  std::vector<double> slope;  // s_j, bits per weight
+  double imp(int64_t b) const { return rho.empty() ? 1.0 * abar[b % G] : rho[b / G] * abar[b % G]; }
+};
 
-int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_report* rep) {
-  if (!d || !rob || !d->rungs || !d->col_importance) return SEEDQ_EINVAL;
+int prepare(const seedq_schedule_desc* d, Prepared& p) {
+  if (!d || !d->rungs || !d->col_importance) return SEEDQ_EINVAL;
   if (d->C != kC) return SEEDQ_EUNSUPPORTED;
   if (d->nrows <= 0 || d->ncols <= 0 || d->ncols % kC != 0) return SEEDQ_EINVAL;
   if (d->nrungs < 1 || d->nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
@@ -60,22 +71,16 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
     for (int r = 0; r < R; ++r)
       if (!std::isfinite(d->damage[r])) return SEEDQ_EHULL;
   }
-  if (!(d->floor_fraction >= 0.0 && d->floor_fraction < 1.0)) return SEEDQ_EINVAL;
-  const int64_t nrows = d->nrows, G = d->ncols / kC;
-  if (nrows > (int64_t(1) << 40) / G) return SEEDQ_EINVAL;
-  const int64_t nb = nrows * G;
-
-  const double budget_f = 8.0 * d->target_bpw * double(nb);
-  if (!std::isfinite(budget_f) || budget_f < 0.0 || budget_f >= 9.0e18 ||
-      budget_f != std::floor(budget_f))
-    return SEEDQ_ERATE;
-  const int64_t budget = int64_t(budget_f);
-
-  std::vector<double> bits(R);
-  for (int r = 0; r < R; ++r) bits[r] = double(d->rungs[r].K + 4 * d->rungs[r].P + 4);
+  p.nrows = d->nrows;
+  p.G = d->ncols / kC;
+  if (p.nrows > (int64_t(1) << 40) / p.G) return SEEDQ_EINVAL;
+  p.nb = p.nrows * p.G;
+  p.bits.resize(R);
+  for (int r = 0; r < R; ++r) p.bits[r] = double(d->rungs[r].K + 4 * d->rungs[r].P + 4);
 
   // ---- importance (eq. (imp)), fixed evaluation order
-  std::vector<double> abar(G);
+  const int64_t G = p.G, nrows = p.nrows;
+  p.abar.assign(G, 0.0);
   for (int64_t g = 0; g < G; ++g) {
     double s = 0.0;
     for (int j = 0; j < kC; ++j) {
@@ -83,15 +88,15 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
       if (!(a > 0.0) || !std::isfinite(a)) return SEEDQ_EINVAL;
       s = s + a;
     }
-    abar[g] = s / 8.0;
+    p.abar[g] = s / 8.0;
   }
   double tot = 0.0;
-  for (int64_t g = 0; g < G; ++g) tot = tot + abar[g];
+  for (int64_t g = 0; g < G; ++g) tot = tot + p.abar[g];
   const double amean = tot / double(G);
-  for (int64_t g = 0; g < G; ++g) abar[g] = abar[g] / amean;
-  std::vector<double> rho;
+  for (int64_t g = 0; g < G; ++g) p.abar[g] = p.abar[g] / amean;
+  p.rho.clear();
   if (d->row_importance) {
-    rho.resize(nrows);
+    p.rho.resize(nrows);
     double tr = 0.0;
     for (int64_t r = 0; r < nrows; ++r) {
       const double v = double(d->row_importance[r]);
@@ -99,12 +104,63 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
       tr = tr + v;
     }
     const double rmean = tr / double(nrows);
-    for (int64_t r = 0; r < nrows; ++r) rho[r] = double(d->row_importance[r]) / rmean;
+    for (int64_t r = 0; r < nrows; ++r) p.rho[r] = double(d->row_importance[r]) / rmean;
   }
-  auto imp_of = [&](int64_t b) -> double {
-    const double a = abar[b % G];
-    return rho.empty() ? 1.0 * a : rho[b / G] * a;
-  };
+
+  // ---- hull (section 3.4)
+  const std::vector<double>& bits = p.bits;
+  std::vector<int>& H = p.H;
+  H.clear();
+  if (R == 1) {
+    H.push_back(0);
+  } else {
+    std::vector<int> order(R);
+    for (int r = 0; r < R; ++r) order[r] = r;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+      if (bits[a] != bits[b]) return bits[a] < bits[b];
+      if (d->damage[a] != d->damage[b]) return d->damage[a] < d->damage[b];
+      return a < b;
+    });
+    for (int i : order) {
+      if (!H.empty() && bits[H.back()] == bits[i]) continue;
+      while (H.size() >= 2) {
+        const int a = H[H.size() - 2], b = H.back();
+        const double cross = (bits[b] - bits[a]) * (d->damage[i] - d->damage[a]) -
+                             (d->damage[b] - d->damage[a]) * (bits[i] - bits[a]);
+        if (cross <= 0.0) H.pop_back();
+        else break;
+      }
+      H.push_back(i);
+    }
+    while (H.size() >= 2 && d->damage[H.back()] >= d->damage[H[H.size() - 2]]) H.pop_back();
+  }
+  const int J = int(H.size());
+  if (J < 1) return SEEDQ_EHULL;
+  p.slope.assign(J > 1 ? J - 1 : 0, 0.0);
+  for (int j = 0; j + 1 < J; ++j)
+    p.slope[j] = (d->damage[H[j]] - d->damage[H[j + 1]]) / ((bits[H[j + 1]] - bits[H[j]]) / 8.0);
+  return SEEDQ_OK;
+}
+
+}  // namespace
+
+int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_report* rep) {
+  if (!rob) return SEEDQ_EINVAL;
+  Prepared pr;
+  const int rc = prepare(d, pr);
+  if (rc != SEEDQ_OK) return rc;
+  if (!(d->floor_fraction >= 0.0 && d->floor_fraction < 1.0)) return SEEDQ_EINVAL;
+  const int R = d->nrungs;
+  const int64_t nrows = pr.nrows, G = pr.G, nb = pr.nb;
+  const double budget_f = 8.0 * d->target_bpw * double(nb);
+  if (!std::isfinite(budget_f) || budget_f < 0.0 || budget_f >= 9.0e18 ||
+      budget_f != std::floor(budget_f))
+    return SEEDQ_ERATE;
+  const int64_t budget = int64_t(budget_f);
+  const std::vector<double>& bits = pr.bits;
+  const std::vector<double>& abar = pr.abar;
+  const std::vector<double>& rho = pr.rho;
+  auto imp_of = [&](int64_t b) -> double { return pr.imp(b); };
 
   // ---- floor (section 3.3)
   int64_t kq = int64_t(std::ceil(double(nb) * d->floor_fraction)) - 1;
@@ -150,36 +206,9 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
   }
   const int ncls = int(cls_val.size());
 
-  // ---- hull (section 3.4)
-  std::vector<int> H;
-  if (R == 1) {
-    H.push_back(0);
-  } else {
-    std::vector<int> order(R);
-    for (int r = 0; r < R; ++r) order[r] = r;
-    std::sort(order.begin(), order.end(), [&](int a, int b) {
-      if (bits[a] != bits[b]) return bits[a] < bits[b];
-      if (d->damage[a] != d->damage[b]) return d->damage[a] < d->damage[b];
-      return a < b;
-    });
-    for (int i : order) {
-      if (!H.empty() && bits[H.back()] == bits[i]) continue;
-      while (H.size() >= 2) {
-        const int a = H[H.size() - 2], b = H.back();
-        const double cross = (bits[b] - bits[a]) * (d->damage[i] - d->damage[a]) -
-                             (d->damage[b] - d->damage[a]) * (bits[i] - bits[a]);
-        if (cross <= 0.0) H.pop_back();
-        else break;
-      }
-      H.push_back(i);
-    }
-    while (H.size() >= 2 && d->damage[H.back()] >= d->damage[H[H.size() - 2]]) H.pop_back();
-  }
+  const std::vector<int>& H = pr.H;
   const int J = int(H.size());
-  if (J < 1) return SEEDQ_EHULL;
-  std::vector<double> slope(J > 1 ? J - 1 : 0);
-  for (int j = 0; j + 1 < J; ++j)
-    slope[j] = (d->damage[H[j]] - d->damage[H[j + 1]]) / ((bits[H[j + 1]] - bits[H[j]]) / 8.0);
+  const std::vector<double>& slope = pr.slope;
 
   if (double(nb) * bits[H[0]] > double(budget)) return SEEDQ_ERATE;
 
@@ -326,6 +355,72 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
     for (int r = 0; r < R; ++r) rep->count[r] = count[r];
     for (int j = 0; j < J; ++j) rep->on_hull[H[j]] = 1;
     rep->nhull = J;
+  }
+  return SEEDQ_OK;
+}
+
+// Decoder side of Algorithm 2: the same importance, floor value and hull as the
+// encoder, the ladder at the stored lambda, and the first T blocks (row-major)
+// that sit exactly at a threshold -- promoted at lambda but not at the next
+// larger double -- taking the lower rung. With the lambda, floor value and tie
+// count that plan_schedule reports, this reproduces its allocation exactly.
+int derive_schedule(const seedq_schedule_desc* d, double lam, double qf, int64_t T, uint8_t* rob) {
+  if (!rob) return SEEDQ_EINVAL;
+  if (!(lam >= 0.0) || !std::isfinite(lam) || !std::isfinite(qf) || T < 0) return SEEDQ_EINVAL;
+  Prepared pr;
+  const int rc = prepare(d, pr);
+  if (rc != SEEDQ_OK) return rc;
+  const int64_t nrows = pr.nrows, G = pr.G, nb = pr.nb;
+  const std::vector<int>& H = pr.H;
+  const int J = int(H.size());
+  const std::vector<double>& slope = pr.slope;
+
+  const double lam_up = std::nextafter(lam, INFINITY);
+  auto position = [&](double l, double v) {
+    int pos = 0;
+    for (int j = 0; j + 1 < J; ++j) pos += (l / slope[j] <= v) ? 1 : 0;
+    return pos;
+  };
+  if (pr.rho.empty()) {
+    std::vector<uint8_t> row(G), lower(G);
+    std::vector<char> tied(G);
+    int64_t ntied = 0;
+    for (int64_t g = 0; g < G; ++g) {
+      const double v = std::max(1.0 * pr.abar[g], qf);
+      const int p = position(lam, v), pu = position(lam_up, v);
+      row[g] = uint8_t(H[p]);
+      lower[g] = uint8_t(H[pu]);
+      tied[g] = p != pu;
+      ntied += tied[g] ? nrows : 0;
+    }
+    if (T > ntied) return SEEDQ_EINVAL;
+    for (int64_t r = 0; r < nrows; ++r) std::memcpy(rob + r * G, row.data(), size_t(G));
+    int64_t left = T;
+    for (int64_t r = 0; r < nrows && left > 0; ++r)
+      for (int64_t g = 0; g < G && left > 0; ++g)
+        if (tied[g]) {
+          rob[r * G + g] = lower[g];
+          --left;
+        }
+  } else {
+    std::vector<uint8_t> pos(nb), pos_up(nb);
+    int64_t ntied = 0;
+    for (int64_t b = 0; b < nb; ++b) {
+      const double v = std::max(pr.imp(b), qf);
+      pos[b] = uint8_t(position(lam, v));
+      pos_up[b] = uint8_t(position(lam_up, v));
+      ntied += pos[b] != pos_up[b] ? 1 : 0;
+    }
+    if (T > ntied) return SEEDQ_EINVAL;
+    int64_t left = T;
+    for (int64_t b = 0; b < nb; ++b) {
+      int p = pos[b];
+      if (left > 0 && pos_up[b] != p) {
+        p = pos_up[b];
+        --left;
+      }
+      rob[b] = uint8_t(H[p]);
+    }
   }
   return SEEDQ_OK;
 }

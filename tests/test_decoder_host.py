@@ -1,0 +1,99 @@
+"""Decoder-side allocation (Algorithm 2): seedq_derive_schedule re-derives every
+block's rung from the stored lambda, floor value and tie count, and must agree
+exactly with the encoder's planner and with the oracle's decoder."""
+import numpy as np
+import pytest
+
+import synthetic
+
+
+@pytest.fixture(scope="module")
+def sq():
+    import os
+    import paper_2609_38477_amd as sq
+    if not os.path.exists(sq.LIB_PATH):
+        from paper_2609_38477_amd import build
+        build.build()
+    return sq
+
+
+RUNGS = ((12, 2), (16, 3), (20, 4))
+DAMAGE = (4.0, 1.0, 0.25)
+
+
+def _roundtrip(sq, oq, nrows, ncols, rungs, damage, target, a, rho=None, f=0.06):
+    enc, rep = sq.plan_schedule(nrows, ncols, rungs, damage, target, a, rho, f)
+    dec = sq.derive_schedule(nrows, ncols, rungs, damage, a, rep["lam"], rep["floor_q"],
+                             rep["tie_count"], rho)
+    assert np.array_equal(dec, enc)
+    ref = oq.schedule(nrows, ncols, rungs, damage, target, a, rho, f)
+    rates = np.array([K + 4 * P + 4 for K, P in rungs], dtype=np.float64)
+    odec = oq.decode_rungs(ref.imp, ref.lam, ref.tie_count, ref.hull, (rates, np.asarray(damage)))
+    assert np.array_equal(odec, dec)
+    return enc, rep
+
+
+@pytest.mark.parametrize("trial", range(12))
+def test_derive_matches_planner_and_oracle_random(sq, oq, trial):
+    rng = np.random.default_rng(300 + trial)
+    nrows = int(rng.integers(1, 6))
+    ncols = 8 * int(rng.integers(1, 12))
+    a = np.exp(rng.normal(0, 1, ncols)).astype(np.float32)
+    if trial % 3 == 0:
+        a = np.round(a * 4).clip(1).astype(np.float32)       # exact ties between groups
+    rho = np.exp(rng.normal(0, 0.5, nrows)).astype(np.float32) if trial % 2 else None
+    nb = nrows * ncols // 8
+    k = int(rng.integers(24 * nb // 8, 40 * nb // 8 + 1))
+    while 8.0 * (k * 8 / (8 * nb)) * nb != 8 * k:      # a budget the planner accepts
+        k += 1
+    target = k * 8 / (8 * nb)
+    _roundtrip(sq, oq, nrows, ncols, RUNGS, DAMAGE, target, a, rho,
+               f=float(rng.choice([0.0, 0.06, 0.3])))
+
+
+def test_derive_tie_split(sq, oq):
+    a = synthetic.importance_profile(32)
+    nb = 12
+    enc, rep = _roundtrip(sq, oq, 3, 32, RUNGS, DAMAGE, (24 * nb + 40) / (8 * nb), a, f=0.0)
+    assert rep["tie_count"] > 0
+    # the tie count is part of what the decoder must hold: another count moves
+    # exactly one tied block per unit
+    other = sq.derive_schedule(3, 32, RUNGS, DAMAGE, a, rep["lam"], rep["floor_q"],
+                               rep["tie_count"] - 1)
+    assert np.count_nonzero(other != enc) == 1
+
+
+@pytest.mark.parametrize("name", ["mlp_up", "l70b"])
+def test_derive_full_size(sq, name):
+    wl = synthetic.WORKLOADS[name]
+    a = synthetic.importance_profile(wl.ncols)
+    enc, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
+    dec = sq.derive_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, a, rep["lam"],
+                             rep["floor_q"], rep["tie_count"])
+    assert np.array_equal(dec, enc)
+
+
+def test_derive_full_size_with_rows(sq):
+    wl = synthetic.WORKLOADS["reduced"]
+    a = synthetic.importance_profile(wl.ncols)
+    rho = np.exp(synthetic.normal(7, synthetic.STREAM_MISC, wl.nrows) * 0.3).astype(np.float32)
+    enc, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a, rho)
+    dec = sq.derive_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, a, rep["lam"],
+                             rep["floor_q"], rep["tie_count"], rho)
+    assert np.array_equal(dec, enc)
+
+
+def test_derive_errors(sq):
+    a = synthetic.importance_profile(64)
+    enc, rep = sq.plan_schedule(4, 64, RUNGS, DAMAGE, 4.0, a)
+    for lam, q, T in ((-1.0, rep["floor_q"], 0), (float("nan"), rep["floor_q"], 0),
+                      (rep["lam"], float("inf"), 0), (rep["lam"], rep["floor_q"], -1),
+                      (rep["lam"], rep["floor_q"], 10 ** 9)):
+        out = np.full(enc.size, 77, dtype=np.uint8)
+        with pytest.raises(sq.SeedqError) as e:
+            sq.derive_schedule(4, 64, RUNGS, DAMAGE, a, lam, q, T, out=out)
+        assert e.value.code == -1
+        assert np.all(out == 77)          # nothing written on error
+    with pytest.raises(sq.SeedqError) as e:
+        sq.derive_schedule(4, 64, RUNGS, None, a, rep["lam"], rep["floor_q"], 0)
+    assert e.value.code == -4
