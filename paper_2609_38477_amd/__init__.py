@@ -90,6 +90,19 @@ def lib() -> ctypes.CDLL:
         L.seedq_decompress.restype = ctypes.c_int
         L.seedq_decompress.argtypes = [vp, vp, vp, vp, i32, ctypes.POINTER(Rung), i64, i64, i32,
                                        vp, vp, vp]
+        L.seedq_stream_bytes.restype = ctypes.c_int
+        L.seedq_stream_bytes.argtypes = [i32, ctypes.POINTER(Rung), vp, ctypes.POINTER(sz)]
+        L.seedq_stream_workspace_bytes.restype = sz
+        L.seedq_stream_workspace_bytes.argtypes = [i64, i64, i32]
+        L.seedq_pack.restype = ctypes.c_int
+        L.seedq_pack.argtypes = [vp, vp, vp, vp, i32, ctypes.POINTER(Rung), i64, i64, i32, vp, sz,
+                                 vp, sz, vp]
+        L.seedq_unpack.restype = ctypes.c_int
+        L.seedq_unpack.argtypes = [vp, sz, vp, i32, ctypes.POINTER(Rung), i64, i64, i32, vp, vp, vp,
+                                   vp, sz, vp]
+        L.seedq_decompress_stream.restype = ctypes.c_int
+        L.seedq_decompress_stream.argtypes = [vp, sz, vp, i32, ctypes.POINTER(Rung), i64, i64, i32,
+                                              vp, vp, sz, vp]
         _lib = L
     return _lib
 
@@ -169,6 +182,47 @@ def seedq_decompress(d_seed, d_exp, d_q, d_rung_of_block, rungs, nrows: int, nco
                                 len(rungs), arr, nrows, ncols, C, _ptr(d_W_hat), _ptr(d_acc),
                                 _stream(stream))
     _check(rc, "seedq_decompress")
+
+
+def _rungs(rungs):
+    return (Rung * len(rungs))(*[Rung(int(K), int(P)) for K, P in rungs])
+
+
+def seedq_stream_bytes(rungs, count_per_rung) -> int:
+    cnt = np.ascontiguousarray(count_per_rung, dtype=np.int64)
+    out = ctypes.c_size_t(0)
+    _check(lib().seedq_stream_bytes(len(rungs), _rungs(rungs), cnt.ctypes.data, ctypes.byref(out)),
+           "seedq_stream_bytes")
+    return int(out.value)
+
+
+def seedq_stream_workspace_bytes(nrows: int, ncols: int, C: int = SEEDQ_BLOCK) -> int:
+    return int(lib().seedq_stream_workspace_bytes(nrows, ncols, C))
+
+
+def seedq_pack(d_seed, d_exp, d_q, d_rung_of_block, rungs, nrows: int, ncols: int, C: int,
+               d_stream, stream_bytes: int, d_workspace, workspace_bytes: int, stream=None) -> None:
+    rc = lib().seedq_pack(_ptr(d_seed), _ptr(d_exp), _ptr(d_q), _ptr(d_rung_of_block), len(rungs),
+                          _rungs(rungs), nrows, ncols, C, _ptr(d_stream), stream_bytes,
+                          _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_pack")
+
+
+def seedq_unpack(d_stream, stream_bytes: int, d_rung_of_block, rungs, nrows: int, ncols: int,
+                 C: int, d_seed, d_exp, d_q, d_workspace, workspace_bytes: int, stream=None) -> None:
+    rc = lib().seedq_unpack(_ptr(d_stream), stream_bytes, _ptr(d_rung_of_block), len(rungs),
+                            _rungs(rungs), nrows, ncols, C, _ptr(d_seed), _ptr(d_exp), _ptr(d_q),
+                            _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_unpack")
+
+
+def seedq_decompress_stream(d_stream, stream_bytes: int, d_rung_of_block, rungs, nrows: int,
+                            ncols: int, C: int, d_W_hat, d_workspace, workspace_bytes: int,
+                            stream=None) -> None:
+    rc = lib().seedq_decompress_stream(_ptr(d_stream), stream_bytes, _ptr(d_rung_of_block),
+                                       len(rungs), _rungs(rungs), nrows, ncols, C, _ptr(d_W_hat),
+                                       _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_decompress_stream")
 
 
 # ---------------------------------------------------------------- helpers
@@ -270,3 +324,50 @@ def decompress(seed, exp, q, rungs, nrows: int, ncols: int, rung_of_block=None,
     seedq_decompress(seed, exp, q, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK, W_hat, acc,
                      stream)
     return W_hat, acc
+
+
+def _stream_ws(nrows, ncols, dev):
+    import torch
+    n = seedq_stream_workspace_bytes(nrows, ncols)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=dev), n
+
+
+def pack(seed, exp, q, rungs, nrows: int, ncols: int, rung_of_block=None, count_per_rung=None,
+         stream=None):
+    """Payload words (torch uint32-as-int32 tensor) of the codes. The length comes
+    from count_per_rung (blocks per rung), by default every block at rungs[0]."""
+    import torch
+    nb = nrows * ncols // SEEDQ_BLOCK
+    if count_per_rung is None:
+        assert len(rungs) == 1
+        count_per_rung = [nb]
+    nbytes = seedq_stream_bytes(rungs, count_per_rung)
+    dev = seed.device
+    words = torch.empty(max(nbytes // 4, 1), dtype=torch.int32, device=dev)
+    ws, nws = _stream_ws(nrows, ncols, dev)
+    seedq_pack(seed, exp, q, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK, words, nbytes, ws, nws,
+               stream)
+    return words[: nbytes // 4]
+
+
+def unpack(words, rungs, nrows: int, ncols: int, rung_of_block=None, stream=None):
+    import torch
+    nb = nrows * ncols // SEEDQ_BLOCK
+    dev = words.device
+    seed = torch.empty(nb, dtype=torch.int32, device=dev)
+    exp = torch.empty(nb, dtype=torch.uint8, device=dev)
+    q = torch.empty((nb, SEEDQ_QSTRIDE), dtype=torch.int8, device=dev)
+    ws, nws = _stream_ws(nrows, ncols, dev)
+    seedq_unpack(words, words.numel() * 4, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK, seed,
+                 exp, q, ws, nws, stream)
+    return seed, exp, q
+
+
+def decompress_stream(words, rungs, nrows: int, ncols: int, rung_of_block=None, stream=None):
+    import torch
+    dev = words.device
+    W_hat = torch.empty((nrows, ncols), dtype=torch.float32, device=dev)
+    ws, nws = _stream_ws(nrows, ncols, dev)
+    seedq_decompress_stream(words, words.numel() * 4, rung_of_block, rungs, nrows, ncols,
+                            SEEDQ_BLOCK, W_hat, ws, nws, stream)
+    return W_hat

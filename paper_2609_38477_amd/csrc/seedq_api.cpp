@@ -123,3 +123,108 @@ int seedq_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t*
 }
 
 }  // extern "C"
+
+namespace {
+
+// Rung table of a decoder call; SEEDQ_OK or the error code.
+int rung_table(int32_t nrungs, const seedq_rung* rungs, RungTable& rt) {
+  if (!rungs || nrungs < 1 || nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
+  std::memset(&rt, 0, sizeof(rt));
+  rt.n = nrungs;
+  for (int r = 0; r < nrungs; ++r) {
+    if (!rung_supported(rungs[r].K, rungs[r].P)) return SEEDQ_EUNSUPPORTED;
+    rt.K[r] = rungs[r].K;
+    rt.P[r] = rungs[r].P;
+  }
+  return SEEDQ_OK;
+}
+
+// Common checks of the stream calls.
+int stream_args(int64_t nrows, int64_t ncols, int32_t C, const void* d_stream, size_t stream_bytes,
+                const uint8_t* d_rung, int32_t nrungs, const seedq_rung* rungs, void* d_ws,
+                size_t ws_bytes, RungTable& rt) {
+  if (C != kC) return SEEDQ_EUNSUPPORTED;
+  if (!d_stream || !shape_ok(nrows, ncols)) return SEEDQ_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(d_stream) & 3u) || (stream_bytes & 3u)) return SEEDQ_EINVAL;
+  const int rc = rung_table(nrungs, rungs, rt);
+  if (rc != SEEDQ_OK) return rc;
+  if (nrungs > 1 && !d_rung) return SEEDQ_EINVAL;
+  if (!d_ws || ws_bytes < stream_workspace_bytes(nrows * (ncols / kC)) ||
+      (reinterpret_cast<uintptr_t>(d_ws) & 255u))
+    return SEEDQ_EWORKSPACE;
+  return SEEDQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int seedq_stream_bytes(int32_t nrungs, const seedq_rung* rungs, const int64_t* count_per_rung,
+                       size_t* bytes) {
+  if (!count_per_rung || !bytes) return SEEDQ_EINVAL;
+  RungTable rt;
+  const int rc = rung_table(nrungs, rungs, rt);
+  if (rc != SEEDQ_OK) return rc;
+  uint64_t bits = 0;
+  for (int r = 0; r < nrungs; ++r) {
+    if (count_per_rung[r] < 0 || count_per_rung[r] > (int64_t(1) << 40)) return SEEDQ_EINVAL;
+    bits += uint64_t(count_per_rung[r]) * uint64_t(rt.K[r] + 4 + 4 * rt.P[r]);
+  }
+  *bytes = size_t((bits + 31) / 32 * 4);
+  return SEEDQ_OK;
+}
+
+size_t seedq_stream_workspace_bytes(int64_t nrows, int64_t ncols, int32_t C) {
+  if (C != kC || !shape_ok(nrows, ncols)) return 0;
+  return stream_workspace_bytes(nrows * (ncols / kC));
+}
+
+int seedq_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+               const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_rung* rungs,
+               int64_t nrows, int64_t ncols, int32_t C, uint32_t* d_stream, size_t stream_bytes,
+               void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+  RungTable rt;
+  const int rc = stream_args(nrows, ncols, C, d_stream, stream_bytes, d_rung_of_block, nrungs,
+                             rungs, d_workspace, workspace_bytes, rt);
+  if (rc != SEEDQ_OK) return rc;
+  if (!d_seed || !d_exp || !d_q || (reinterpret_cast<uintptr_t>(d_q) & 7u)) return SEEDQ_EINVAL;
+  const hipError_t e = launch_pack(d_seed, d_exp, d_q, nrungs > 1 ? d_rung_of_block : nullptr, rt,
+                                   nrows * (ncols / kC), d_stream, int64_t(stream_bytes / 4),
+                                   d_workspace, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_unpack(const uint32_t* d_stream, size_t stream_bytes, const uint8_t* d_rung_of_block,
+                 int32_t nrungs, const seedq_rung* rungs, int64_t nrows, int64_t ncols, int32_t C,
+                 uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, void* d_workspace,
+                 size_t workspace_bytes, void* hip_stream) {
+  RungTable rt;
+  const int rc = stream_args(nrows, ncols, C, d_stream, stream_bytes, d_rung_of_block, nrungs,
+                             rungs, d_workspace, workspace_bytes, rt);
+  if (rc != SEEDQ_OK) return rc;
+  if (!d_seed || !d_exp || !d_q || (reinterpret_cast<uintptr_t>(d_q) & 7u)) return SEEDQ_EINVAL;
+  const hipError_t e = launch_parse(d_stream, int64_t(stream_bytes / 4),
+                                    nrungs > 1 ? d_rung_of_block : nullptr, rt,
+                                    nrows * (ncols / kC), d_workspace, d_seed, d_exp, d_q, nullptr,
+                                    static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_decompress_stream(const uint32_t* d_stream, size_t stream_bytes,
+                            const uint8_t* d_rung_of_block, int32_t nrungs,
+                            const seedq_rung* rungs, int64_t nrows, int64_t ncols, int32_t C,
+                            float* d_W_hat, void* d_workspace, size_t workspace_bytes,
+                            void* hip_stream) {
+  RungTable rt;
+  const int rc = stream_args(nrows, ncols, C, d_stream, stream_bytes, d_rung_of_block, nrungs,
+                             rungs, d_workspace, workspace_bytes, rt);
+  if (rc != SEEDQ_OK) return rc;
+  if (!d_W_hat || (reinterpret_cast<uintptr_t>(d_W_hat) & 15u)) return SEEDQ_EINVAL;
+  const hipError_t e = launch_parse(d_stream, int64_t(stream_bytes / 4),
+                                    nrungs > 1 ? d_rung_of_block : nullptr, rt,
+                                    nrows * (ncols / kC), d_workspace, nullptr, nullptr, nullptr,
+                                    d_W_hat, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+}  // extern "C"

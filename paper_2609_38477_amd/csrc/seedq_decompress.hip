@@ -6,7 +6,7 @@
 // and scales it by 2^-(K-1+e) after a single rounding to fp32. Reads 14 bytes
 // of code per block, writes 32 bytes of weights (+32 of acc); neighbouring
 // threads touch neighbouring 32-byte blocks, so every access is coalesced.
-#include "seedq_internal.h"
+#include "seedq_reconstruct.h"
 
 namespace seedq {
 namespace {
@@ -25,28 +25,13 @@ decompress_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__
   const int e = expo[b];
   ok = ok && s >= 1u && s < (1u << K) && e <= 15;
   const uint2 qw = reinterpret_cast<const uint2*>(q)[b];
-  const uint32_t mask = lfsr_mask(K);
-  const int32_t half = int32_t(1) << (K - 1);
-
   int32_t acc[kC];
-#pragma unroll
-  for (int i = 0; i < kC; ++i) acc[i] = 0;
-  uint32_t x = s;
-  for (int j = 0; j < P; ++j) {
-    const uint32_t word = (j < 4) ? qw.x : qw.y;
-    const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
-#pragma unroll
-    for (int i = 0; i < kC; ++i) {
-      acc[i] += (int32_t(x) - half) * qj;
-      x = lfsr_step(x, mask);
-    }
-  }
-  const int sh = -(K - 1 + e);
+  block_acc(s, K, P, qw, acc);
   float o[kC];
+  block_weights(acc, K, e, ok, o);
+  if (!ok) {
 #pragma unroll
-  for (int i = 0; i < kC; ++i) {
-    o[i] = ok ? ldexpf(__int2float_rn(acc[i]), sh) : __int_as_float(0x7fc00000);
-    if (!ok) acc[i] = 0;
+    for (int i = 0; i < kC; ++i) acc[i] = 0;
   }
   float4* dst = reinterpret_cast<float4*>(W_hat + b * kC);
   dst[0] = make_float4(o[0], o[1], o[2], o[3]);

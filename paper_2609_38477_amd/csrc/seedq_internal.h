@@ -124,6 +124,18 @@ hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const
                              const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
                              float* d_W_hat, int32_t* d_acc, hipStream_t stream);
 
+// Code stream (seedq_stream.hip). The workspace holds one int64 per chunk of
+// 2048 blocks plus one.
+int64_t stream_chunks(int64_t nblocks);
+size_t stream_workspace_bytes(int64_t nblocks);
+hipError_t launch_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+                       const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
+                       uint32_t* d_stream, int64_t nwords, void* d_ws, hipStream_t stream);
+// Codes out when d_W_hat is null, reconstructed weights out otherwise.
+hipError_t launch_parse(const uint32_t* d_stream, int64_t nwords, const uint8_t* d_rung,
+                        const RungTable& rt, int64_t nblocks, void* d_ws, uint32_t* d_seed,
+                        uint8_t* d_exp, int8_t* d_q, float* d_W_hat, hipStream_t stream);
+
 // Host planner (seedq_schedule.cpp).
 int derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,
                     int64_t tie_count, uint8_t* rung_of_block);

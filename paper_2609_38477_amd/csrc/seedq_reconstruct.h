@@ -1,0 +1,38 @@
+// Exact reconstruction of one block from its code (section 3.1 eq. (codec),
+// Algorithm 2): regenerate the 8P LFSR states of seed s, form the integer
+// products acc_i = sum_j U_int[i][j] q_j (|acc| < 2^29) and scale by
+// 2^-(K-1+e) after one rounding to fp32. Shared by the decoders.
+#pragma once
+
+#include "seedq_internal.h"
+
+namespace seedq {
+
+// q_j is the signed byte j of qw (bytes 0-3 in qw.x, 4-7 in qw.y).
+__device__ __forceinline__ void block_acc(uint32_t s, int K, int P, uint2 qw, int32_t (&acc)[kC]) {
+  const uint32_t mask = lfsr_mask(K);
+  const int32_t half = int32_t(1) << (K - 1);
+#pragma unroll
+  for (int i = 0; i < kC; ++i) acc[i] = 0;
+  uint32_t x = s;
+  for (int j = 0; j < P; ++j) {
+    const uint32_t word = (j < 4) ? qw.x : qw.y;
+    const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      acc[i] += (int32_t(x) - half) * qj;
+      x = lfsr_step(x, mask);
+    }
+  }
+}
+
+// w_hat_i = acc_i 2^-(K-1+e), NaN for an invalid code.
+__device__ __forceinline__ void block_weights(const int32_t (&acc)[kC], int K, int e, bool ok,
+                                              float (&o)[kC]) {
+  const int sh = -(K - 1 + e);
+#pragma unroll
+  for (int i = 0; i < kC; ++i)
+    o[i] = ok ? ldexpf(__int2float_rn(acc[i]), sh) : __int_as_float(0x7fc00000);
+}
+
+}  // namespace seedq

@@ -1,0 +1,280 @@
+// The headerless variable-length code stream of one tensor (Algorithm 1, the
+// emit step: every block contributes exactly l(g_b) = K + 4P + 4 bits of
+// eq. (rate), with no header; Algorithm 2 and the appendix on encoding and
+// decoding: blocks are parsed left to right inside a tensor, their lengths
+// known from the allocation alone).
+//
+// Layout: blocks in row-major order; inside a block the seed (K bits), the
+// exponent (4 bits) and the mantissas q_0 .. q_{P-1} (4 bits each, two's
+// complement), every field least-significant bit first at increasing stream
+// bit positions; stream bit n is bit n % 32 of 32-bit word n / 32; the payload
+// is padded with zero bits to a whole word.
+//
+// Every kernel walks the blocks in chunks of 2048 (one workgroup each): a first
+// pass sums the lengths of every chunk, one workgroup turns the sums into the
+// bit offset of every chunk, and the chunk's workgroup then finds each block's
+// offset with workgroup prefix sums over its rung lengths (256 blocks at a
+// time, so neighbouring threads handle neighbouring blocks and every global
+// access is coalesced). The packer assembles its chunk in LDS and stores whole
+// words; only the two words a chunk may share with its neighbours are merged
+// with atomic ORs (they are cleared by the offset pass).
+#include "seedq_reconstruct.h"
+
+namespace seedq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kIters = 8;
+constexpr int kChunk = kThreads * kIters;  // blocks per workgroup
+constexpr int kMaxBlockBits = SEEDQ_MAX_K + 4 + 4 * SEEDQ_MAX_P;
+// bit 31 + every bit of a chunk, plus the two words a code may spill into
+constexpr int kStageWords = (31 + kChunk * kMaxBlockBits) / 32 + 3;
+
+__device__ __forceinline__ int code_bits(const RungTable& rt, int r) {
+  return r < rt.n ? rt.K[r] + 4 + 4 * rt.P[r] : 0;
+}
+
+// Exclusive prefix sum of v over the workgroup; *total receives the sum.
+__device__ uint32_t wg_exclusive_scan(uint32_t v, uint32_t* total) {
+  __shared__ uint32_t wsum[kThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) {
+    const uint32_t s = wsum[w];
+    before += (w < wave) ? s : 0u;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
+}
+
+__global__ void __launch_bounds__(kThreads)
+chunk_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nblocks,
+                  int64_t* __restrict__ chunk) {
+  const int64_t base = int64_t(blockIdx.x) * kChunk;
+  uint32_t sum = 0;
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t b = base + it * kThreads + threadIdx.x;
+    if (b < nblocks) sum += code_bits(rt, rung ? int(rung[b]) : 0);
+  }
+  uint32_t tot;
+  wg_exclusive_scan(sum, &tot);
+  if (threadIdx.x == 0) chunk[blockIdx.x] = tot;
+}
+
+// One workgroup: chunk[c] (bits of chunk c) -> chunk[c] = bit offset of chunk c,
+// chunk[nchunks] = total bits, in place. With a stream, also clears the words
+// that hold a chunk boundary, the only words two chunks both write.
+__global__ void __launch_bounds__(kThreads)
+chunk_offsets_kernel(int64_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ stream,
+                     int64_t nwords) {
+  __shared__ int64_t part[kThreads];
+  const int64_t per = (nchunks + kThreads - 1) / kThreads;
+  const int64_t c0 = min(nchunks, int64_t(threadIdx.x) * per);
+  const int64_t c1 = min(nchunks, c0 + per);
+  int64_t s = 0;
+  for (int64_t c = c0; c < c1; ++c) s += chunk[c];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int t = 0; t < kThreads; ++t) {
+      const int64_t v = part[t];
+      part[t] = run;
+      run += v;
+    }
+    chunk[nchunks] = run;
+  }
+  __syncthreads();
+  int64_t run = part[threadIdx.x];
+  for (int64_t c = c0; c < c1; ++c) {
+    const int64_t v = chunk[c];
+    chunk[c] = run;
+    if (stream && (run >> 5) < nwords) stream[run >> 5] = 0u;
+    run += v;
+  }
+  if (stream && threadIdx.x == 0 && (chunk[nchunks] >> 5) < nwords) stream[chunk[nchunks] >> 5] = 0u;
+}
+
+__global__ void __launch_bounds__(kThreads)
+pack_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
+            const int8_t* __restrict__ q, const uint8_t* __restrict__ rung, RungTable rt,
+            int64_t nblocks, const int64_t* __restrict__ chunk, uint32_t* __restrict__ stream,
+            int64_t nwords) {
+  __shared__ uint32_t stage[kStageWords];
+  const int64_t base = int64_t(blockIdx.x) * kChunk;
+  const int64_t off0 = chunk[blockIdx.x], off1 = chunk[blockIdx.x + 1];
+  const int64_t w0 = off0 >> 5;
+  const uint32_t shift = uint32_t(off0 & 31);
+  const int nw = int((off1 - (w0 << 5) + 31) >> 5);
+  for (int i = threadIdx.x; i < nw; i += kThreads) stage[i] = 0u;
+  __syncthreads();
+  uint32_t run = shift;  // bit position inside stage
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t b = base + it * kThreads + threadIdx.x;
+    const int r = b < nblocks ? (rung ? int(rung[b]) : 0) : SEEDQ_MAX_RUNGS;
+    const uint32_t len = b < nblocks ? uint32_t(code_bits(rt, r)) : 0u;
+    uint32_t tot;
+    const uint32_t ex = wg_exclusive_scan(len, &tot);
+    if (len) {
+      const int K = rt.K[r], P = rt.P[r];
+      uint64_t code = uint64_t(seed[b] & ((1u << K) - 1u)) | (uint64_t(expo[b] & 15u) << K);
+      const uint2 qw = reinterpret_cast<const uint2*>(q)[b];
+      for (int j = 0; j < P; ++j) {
+        const uint32_t word = j < 4 ? qw.x : qw.y;
+        code |= uint64_t((word >> (8 * (j & 3))) & 15u) << (K + 4 + 4 * j);
+      }
+      const uint32_t pos = run + ex;
+      const int wi = int(pos >> 5), sh = int(pos & 31);
+      const uint64_t lo = code << sh;
+      const uint32_t hi = sh ? uint32_t(code >> (64 - sh)) : 0u;
+      atomicOr(&stage[wi], uint32_t(lo));
+      if (uint32_t(lo >> 32)) atomicOr(&stage[wi + 1], uint32_t(lo >> 32));
+      if (hi) atomicOr(&stage[wi + 2], hi);
+    }
+    run += tot;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nw; i += kThreads) {
+    const int64_t gw = w0 + i;
+    if (gw < nwords) {
+      const bool shared = (i == 0 && shift != 0) || (i == nw - 1 && (off1 & 31) != 0);
+      if (shared) atomicOr(&stream[gw], stage[i]);
+      else stream[gw] = stage[i];
+    }
+  }
+}
+
+// Code of the block whose len bits start at stream bit pos (len <= 52), or
+// false when the stream ends before it.
+__device__ __forceinline__ bool read_code(const uint32_t* __restrict__ stream, int64_t nwords,
+                                          int64_t pos, int len, uint64_t& code) {
+  if (pos + len > (nwords << 5)) return false;
+  const int64_t wi = pos >> 5;
+  const int sh = int(pos & 31);
+  const uint32_t a = stream[wi];
+  const uint32_t b = wi + 1 < nwords ? stream[wi + 1] : 0u;
+  const uint32_t c = wi + 2 < nwords ? stream[wi + 2] : 0u;
+  uint64_t v = ((uint64_t(b) << 32) | a) >> sh;
+  if (sh) v |= uint64_t(c) << (64 - sh);
+  code = v & ((uint64_t(1) << len) - 1u);
+  return true;
+}
+
+// Fields of a code: seed, exponent and the mantissas as signed bytes of qw.
+__device__ __forceinline__ void split_code(uint64_t code, int K, int P, uint32_t& s, int& e,
+                                           uint2& qw) {
+  s = uint32_t(code & ((uint64_t(1) << K) - 1u));
+  e = int((code >> K) & 15u);
+  qw = make_uint2(0u, 0u);
+  for (int j = 0; j < P; ++j) {
+    const uint32_t v = uint32_t((code >> (K + 4 + 4 * j)) & 15u);
+    const uint32_t byte = (v ^ 8u) - 8u;  // sign-extend the nibble
+    if (j < 4) qw.x |= (byte & 0xFFu) << (8 * j);
+    else qw.y |= (byte & 0xFFu) << (8 * (j - 4));
+  }
+}
+
+// MODE 0: codes out (seed, exp, q); MODE 1: reconstructed weights out.
+template <int MODE>
+__global__ void __launch_bounds__(kThreads)
+parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t* __restrict__ rung,
+             RungTable rt, int64_t nblocks, const int64_t* __restrict__ chunk,
+             uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
+             int8_t* __restrict__ q_out, float* __restrict__ W_hat) {
+  const int64_t base = int64_t(blockIdx.x) * kChunk;
+  int64_t run = chunk[blockIdx.x];
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t b = base + it * kThreads + threadIdx.x;
+    const int r = b < nblocks ? (rung ? int(rung[b]) : 0) : SEEDQ_MAX_RUNGS;
+    const int len = b < nblocks ? code_bits(rt, r) : 0;
+    uint32_t tot;
+    const uint32_t ex = wg_exclusive_scan(uint32_t(len), &tot);
+    if (b < nblocks) {
+      const int K = len ? rt.K[r] : SEEDQ_MIN_K;
+      const int P = len ? rt.P[r] : 1;
+      uint64_t code = 0;
+      const bool ok = len && read_code(stream, nwords, run + ex, len, code);
+      uint32_t s = 0u;
+      int e = 0;
+      uint2 qw = make_uint2(0u, 0u);
+      if (ok) split_code(code, K, P, s, e, qw);
+      if (MODE == 0) {
+        seed_out[b] = s;
+        exp_out[b] = uint8_t(e);
+        reinterpret_cast<uint2*>(q_out)[b] = qw;
+      } else {
+        int32_t acc[kC];
+        block_acc(ok ? s : 1u, K, P, qw, acc);
+        float o[kC];
+        block_weights(acc, K, e, ok && s != 0u, o);
+        float4* dst = reinterpret_cast<float4*>(W_hat + b * kC);
+        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+        dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+      }
+    }
+    run += tot;
+  }
+}
+
+}  // namespace
+
+int64_t stream_chunks(int64_t nblocks) { return (nblocks + kChunk - 1) / kChunk; }
+
+size_t stream_workspace_bytes(int64_t nblocks) {
+  return align256(sizeof(int64_t) * size_t(stream_chunks(nblocks) + 1));
+}
+
+static hipError_t launch_offsets(const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
+                                 int64_t* chunk, uint32_t* zero_stream, int64_t nwords,
+                                 hipStream_t stream) {
+  const int64_t nchunks = stream_chunks(nblocks);
+  if (nchunks > 0)
+    hipLaunchKernelGGL(chunk_bits_kernel, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_rung,
+                       rt, nblocks, chunk);
+  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kThreads), 0, stream, chunk, nchunks,
+                     zero_stream, nwords);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
+                       const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
+                       uint32_t* d_stream, int64_t nwords, void* d_ws, hipStream_t stream) {
+  int64_t* chunk = static_cast<int64_t*>(d_ws);
+  hipError_t err = launch_offsets(d_rung, rt, nblocks, chunk, d_stream, nwords, stream);
+  if (err != hipSuccess) return err;
+  const int64_t nchunks = stream_chunks(nblocks);
+  if (nchunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_kernel, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_seed, d_exp,
+                     d_q, d_rung, rt, nblocks, chunk, d_stream, nwords);
+  return hipGetLastError();
+}
+
+hipError_t launch_parse(const uint32_t* d_stream, int64_t nwords, const uint8_t* d_rung,
+                        const RungTable& rt, int64_t nblocks, void* d_ws, uint32_t* d_seed,
+                        uint8_t* d_exp, int8_t* d_q, float* d_W_hat, hipStream_t stream) {
+  int64_t* chunk = static_cast<int64_t*>(d_ws);
+  hipError_t err = launch_offsets(d_rung, rt, nblocks, chunk, nullptr, 0, stream);
+  if (err != hipSuccess) return err;
+  const int64_t nchunks = stream_chunks(nblocks);
+  if (nchunks == 0) return hipSuccess;
+  if (d_W_hat)
+    hipLaunchKernelGGL(parse_kernel<1>, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_stream,
+                       nwords, d_rung, rt, nblocks, chunk, nullptr, nullptr, nullptr, d_W_hat);
+  else
+    hipLaunchKernelGGL(parse_kernel<0>, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_stream,
+                       nwords, d_rung, rt, nblocks, chunk, d_seed, d_exp, d_q, nullptr);
+  return hipGetLastError();
+}
+
+}  // namespace seedq

@@ -31,7 +31,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(sq):
     names = _declared()
-    assert len(names) == 8
+    assert len(names) == 13
     L = ctypes.CDLL(sq.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -144,3 +144,37 @@ def test_planner_errors(sq):
     with pytest.raises(sq.SeedqError) as e:
         sq.plan_schedule(4, 60, ((12, 2),), None, 3.0, a[:60])
     assert e.value.code == -1
+
+
+def test_stream_bytes_is_the_rate_identity(sq):
+    rungs = ((8, 1), (12, 2), (16, 3), (20, 4), (24, 6))
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        cnt = rng.integers(0, 100000, len(rungs))
+        bits = sum(int(c) * (K + 4 * P + 4) for c, (K, P) in zip(cnt, rungs))
+        assert sq.seedq_stream_bytes(rungs, cnt) == (bits + 31) // 32 * 4
+    assert sq.seedq_stream_bytes(((16, 3),), [2 ** 21]) == 2 ** 21 * 32 // 8
+
+
+def test_stream_argument_errors_need_no_gpu(sq):
+    L = sq.lib()
+    R = sq._rungs(((16, 3),))
+    ws = sq.seedq_stream_workspace_bytes(8, 64)
+    assert ws >= 8 * 2 and ws % 256 == 0
+    assert sq.seedq_stream_workspace_bytes(8, 60) == 0
+    # C != 8
+    assert L.seedq_pack(256, 256, 256, None, 1, R, 8, 64, 4, 256, 64, 256, ws, None) == -2
+    # stream not 4-byte aligned / length not a multiple of 4
+    assert L.seedq_pack(256, 256, 256, None, 1, R, 8, 64, 8, 258, 64, 256, ws, None) == -1
+    assert L.seedq_unpack(256, 63, None, 1, R, 8, 64, 8, 256, 256, 256, 256, ws, None) == -1
+    # workspace missing, small or misaligned
+    assert L.seedq_unpack(256, 64, None, 1, R, 8, 64, 8, 256, 256, 256, None, ws, None) == -6
+    assert L.seedq_unpack(256, 64, None, 1, R, 8, 64, 8, 256, 256, 256, 256, ws - 8, None) == -6
+    assert L.seedq_decompress_stream(256, 64, None, 1, R, 8, 64, 8, 256, 260, ws, None) == -6
+    # several rungs without a rung array; unsupported rung
+    R2 = sq._rungs(((12, 2), (16, 3)))
+    assert L.seedq_decompress_stream(256, 64, None, 2, R2, 8, 64, 8, 256, 256, ws, None) == -1
+    assert L.seedq_decompress_stream(256, 64, None, 1, sq._rungs(((25, 3),)), 8, 64, 8, 256, 256,
+                                     ws, None) == -2
+    # W_hat misaligned
+    assert L.seedq_decompress_stream(256, 64, None, 1, R, 8, 64, 8, 264, 256, ws, None) == -1

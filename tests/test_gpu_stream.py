@@ -1,0 +1,145 @@
+"""GPU code stream through the C ABI against the stream oracle.
+
+Bars: packed words, parsed codes and reconstructed weights are bit-exact
+(integer and byte work); NaN marks exactly the blocks the contract names."""
+import os
+
+import numpy as np
+import pytest
+
+import synthetic
+from oracle import stream as ostream
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "stream_three_blocks.txt")
+MIXED = [(8, 1), (12, 2), (16, 3), (20, 4), (24, 6)]
+
+
+@pytest.fixture(scope="module")
+def sq():
+    import paper_2609_38477_amd as sq
+    sq.lib()
+    return sq
+
+
+def _t(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _codes(rng, rob, rungs):
+    nb = len(rob)
+    seed = np.array([int(rng.integers(1, 1 << rungs[r][0])) if r < len(rungs) else 0 for r in rob],
+                    dtype=np.uint32)
+    exp = rng.integers(0, 16, nb).astype(np.uint8)
+    q = np.zeros((nb, 8), dtype=np.int8)
+    for b in range(nb):
+        if rob[b] < len(rungs):
+            q[b, :rungs[rob[b]][1]] = rng.integers(-8, 8, rungs[rob[b]][1])
+    return seed, exp, q
+
+
+def _words(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def test_pack_and_unpack_hand_derived_payload(sq):
+    rob = np.array([0, 1, 0], dtype=np.uint8)
+    rungs = [(8, 2), (9, 3)]
+    seed = np.array([0xA5, 0x1C3, 0x01], dtype=np.uint32)
+    exp = np.array([3, 9, 15], dtype=np.uint8)
+    q = np.zeros((3, 8), dtype=np.int8)
+    q[0, :2], q[1, :3], q[2, :2] = (-1, 5), (7, -8, 0), (2, -3)
+    gold = np.array([0x3C35F3A5, 0xA5E0210F, 0x00000001], dtype=np.uint32)
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), rungs, 1, 24, _t(rob), [2, 1])
+    assert np.array_equal(_words(w), gold)
+    s, e, qq = sq.unpack(_t(gold.view(np.int32)), rungs, 1, 24, _t(rob))
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), seed)
+    assert np.array_equal(e.cpu().numpy(), exp) and np.array_equal(qq.cpu().numpy(), q)
+
+
+@pytest.mark.parametrize("shape", [(5, 8000), (1, 8), (3, 16392), (2, 32768)])
+def test_pack_matches_oracle_mixed_rungs(sq, oq, shape):
+    # several chunks of 2048 blocks with a ragged tail, every rung width, and
+    # blocks with an out-of-range rung index (no bits, seed 0 / NaN on decode)
+    nrows, ncols = shape
+    nb = nrows * ncols // 8
+    rng = np.random.default_rng(nb)
+    rob = rng.integers(0, len(MIXED), nb).astype(np.uint8)
+    rob[rng.random(nb) < 0.02] = 7
+    seed, exp, q = _codes(rng, rob, MIXED)
+    valid = rob < len(MIXED)
+    ref = ostream.pack(seed[valid], exp[valid], q[valid], rob[valid], MIXED)
+    cnt = np.bincount(rob[valid], minlength=len(MIXED))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
+    assert np.array_equal(_words(w), ref)
+    s, e, qq = sq.unpack(w, MIXED, nrows, ncols, _t(rob))
+    s, e, qq = s.cpu().numpy().view(np.uint32), e.cpu().numpy(), qq.cpu().numpy()
+    assert np.array_equal(s[valid], seed[valid]) and np.array_equal(e[valid], exp[valid])
+    assert np.array_equal(qq[valid], q[valid])
+    assert np.all(s[~valid] == 0) and np.all(e[~valid] == 0) and np.all(qq[~valid] == 0)
+    # one-pass decode equals parse + reconstruct, and the oracle's reconstruction
+    Wh = sq.decompress_stream(w, MIXED, nrows, ncols, _t(rob)).cpu().numpy().reshape(-1, 8)
+    K_of = np.array([MIXED[r][0] if r < len(MIXED) else 8 for r in rob])
+    P_of = np.array([MIXED[r][1] if r < len(MIXED) else 1 for r in rob])
+    idx = np.nonzero(valid)[0][:: max(1, nb // 3000)]
+    ref_w, _ = oq.decompress(seed[idx], exp[idx], q[idx], K_of[idx], P_of[idx])
+    assert np.array_equal(Wh[idx], np.asarray(ref_w, dtype=np.float32).reshape(-1, 8))
+    assert np.all(np.isnan(Wh[~valid]))
+
+
+def test_short_stream_marks_only_the_blocks_past_its_end(sq):
+    nrows, ncols = 2, 8 * 3000
+    nb = nrows * ncols // 8
+    rng = np.random.default_rng(9)
+    rob = rng.integers(0, len(MIXED), nb).astype(np.uint8)
+    seed, exp, q = _codes(rng, rob, MIXED)
+    cnt = np.bincount(rob, minlength=len(MIXED))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
+    cut = w[: w.numel() // 2]
+    s, e, qq = sq.unpack(cut, MIXED, nrows, ncols, _t(rob))
+    s = s.cpu().numpy().view(np.uint32)
+    ends = np.cumsum([MIXED[r][0] + 4 + 4 * MIXED[r][1] for r in rob])
+    inside = ends <= 32 * cut.numel()
+    assert inside.any() and (~inside).any()
+    assert np.array_equal(s[inside], seed[inside]) and np.all(s[~inside] == 0)
+    Wh = sq.decompress_stream(cut, MIXED, nrows, ncols, _t(rob)).cpu().numpy().reshape(-1, 8)
+    assert not np.isnan(Wh[inside]).any() and np.isnan(Wh[~inside]).all()
+
+
+def test_full_size_round_trip_from_the_search(sq):
+    # attn4096: real codes from the search, payload of exactly 32 bits per block
+    import torch
+    wl = synthetic.WORKLOADS["attn4096"]
+    W = torch.from_numpy(synthetic.workload_weights(wl)).cuda()
+    b = sq.build_bases(16, 3)
+    seed, exp, q, _ = sq.compress(W, [b])
+    w = sq.pack(seed, exp, q, [(16, 3)], wl.nrows, wl.ncols)
+    assert w.numel() == wl.nblocks
+    s, e, qq = sq.unpack(w, [(16, 3)], wl.nrows, wl.ncols)
+    assert torch.equal(s, seed) and torch.equal(e, exp) and torch.equal(qq, q)
+    W1, _ = sq.decompress(seed, exp, q, [(16, 3)], wl.nrows, wl.ncols)
+    W2 = sq.decompress_stream(w, [(16, 3)], wl.nrows, wl.ncols)
+    assert torch.equal(W1, W2)
+
+
+def test_decoder_path_with_rederived_rungs(sq):
+    # encoder: plan, search, pack; decoder: re-derive the rungs from the stored
+    # lambda / floor / tie count, then parse and reconstruct in one pass
+    import torch
+    wl = synthetic.WORKLOADS["reduced"]
+    nrows = 64
+    a = synthetic.importance_profile(wl.ncols)
+    W = synthetic.weights(nrows, wl.ncols, wl.sigma, 21, wl.outlier_frac)
+    rob, rep = sq.plan_schedule(nrows, wl.ncols, wl.rungs, wl.damage, 3.296875, a, None, 0.06)
+    assert rep["tie_count"] > 0
+    bases = [sq.build_bases(K, P) for K, P in wl.rungs]
+    seed, exp, q, _ = sq.compress(_t(W), bases, _t(rob))
+    words = sq.pack(seed, exp, q, list(wl.rungs), nrows, wl.ncols, _t(rob), rep["count"])
+    dec_rob = sq.derive_schedule(nrows, wl.ncols, wl.rungs, wl.damage, a, rep["lam"], rep["floor_q"],
+                                 rep["tie_count"])
+    assert np.array_equal(dec_rob, rob)
+    Wd = sq.decompress_stream(words, list(wl.rungs), nrows, wl.ncols, _t(dec_rob))
+    Wr, _ = sq.decompress(seed, exp, q, list(wl.rungs), nrows, wl.ncols, _t(rob))
+    assert torch.equal(Wd, Wr)
