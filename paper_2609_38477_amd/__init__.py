@@ -103,6 +103,9 @@ def lib() -> ctypes.CDLL:
         L.seedq_decompress_stream.restype = ctypes.c_int
         L.seedq_decompress_stream.argtypes = [vp, sz, vp, i32, ctypes.POINTER(Rung), i64, i64, i32,
                                               vp, vp, sz, vp]
+        L.seedq_gemv_stream.restype = ctypes.c_int
+        L.seedq_gemv_stream.argtypes = [vp, sz, vp, i32, ctypes.POINTER(Rung), i64, i64, i32, i32,
+                                        vp, vp, vp, sz, vp]
         _lib = L
     return _lib
 
@@ -223,6 +226,15 @@ def seedq_decompress_stream(d_stream, stream_bytes: int, d_rung_of_block, rungs,
                                        len(rungs), _rungs(rungs), nrows, ncols, C, _ptr(d_W_hat),
                                        _ptr(d_workspace), workspace_bytes, _stream(stream))
     _check(rc, "seedq_decompress_stream")
+
+
+def seedq_gemv_stream(d_stream, stream_bytes: int, d_rung_of_block, rungs, nrows: int, ncols: int,
+                      C: int, nvec: int, d_x, d_y, d_workspace, workspace_bytes: int,
+                      stream=None) -> None:
+    rc = lib().seedq_gemv_stream(_ptr(d_stream), stream_bytes, _ptr(d_rung_of_block), len(rungs),
+                                 _rungs(rungs), nrows, ncols, C, nvec, _ptr(d_x), _ptr(d_y),
+                                 _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_gemv_stream")
 
 
 # ---------------------------------------------------------------- helpers
@@ -371,3 +383,16 @@ def decompress_stream(words, rungs, nrows: int, ncols: int, rung_of_block=None, 
     seedq_decompress_stream(words, words.numel() * 4, rung_of_block, rungs, nrows, ncols,
                             SEEDQ_BLOCK, W_hat, ws, nws, stream)
     return W_hat
+
+
+def gemv_stream(words, rungs, nrows: int, ncols: int, x, rung_of_block=None, stream=None):
+    """y = W_hat x with W_hat decoded from the stream; x is fp32 [nvec, ncols]
+    (or [ncols]) on the GPU, nvec in {1, 2, 4, 8}; returns y [nvec, nrows] (or [nrows])."""
+    import torch
+    squeeze = x.dim() == 1
+    xx = x.reshape(-1, ncols).contiguous()
+    y = torch.empty((xx.shape[0], nrows), dtype=torch.float32, device=x.device)
+    ws, nws = _stream_ws(nrows, ncols, x.device)
+    seedq_gemv_stream(words, words.numel() * 4, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK,
+                      xx.shape[0], xx, y, ws, nws, stream)
+    return y[0] if squeeze else y

@@ -149,7 +149,7 @@ int stream_args(int64_t nrows, int64_t ncols, int32_t C, const void* d_stream, s
   const int rc = rung_table(nrungs, rungs, rt);
   if (rc != SEEDQ_OK) return rc;
   if (nrungs > 1 && !d_rung) return SEEDQ_EINVAL;
-  if (!d_ws || ws_bytes < stream_workspace_bytes(nrows * (ncols / kC)) ||
+  if (!d_ws || ws_bytes < stream_workspace_bytes(nrows * (ncols / kC), nrows) ||
       (reinterpret_cast<uintptr_t>(d_ws) & 255u))
     return SEEDQ_EWORKSPACE;
   return SEEDQ_OK;
@@ -176,7 +176,7 @@ int seedq_stream_bytes(int32_t nrungs, const seedq_rung* rungs, const int64_t* c
 
 size_t seedq_stream_workspace_bytes(int64_t nrows, int64_t ncols, int32_t C) {
   if (C != kC || !shape_ok(nrows, ncols)) return 0;
-  return stream_workspace_bytes(nrows * (ncols / kC));
+  return stream_workspace_bytes(nrows * (ncols / kC), nrows);
 }
 
 int seedq_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
@@ -224,6 +224,25 @@ int seedq_decompress_stream(const uint32_t* d_stream, size_t stream_bytes,
                                     nrungs > 1 ? d_rung_of_block : nullptr, rt,
                                     nrows * (ncols / kC), d_workspace, nullptr, nullptr, nullptr,
                                     d_W_hat, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_gemv_stream(const uint32_t* d_stream, size_t stream_bytes, const uint8_t* d_rung_of_block,
+                      int32_t nrungs, const seedq_rung* rungs, int64_t nrows, int64_t ncols,
+                      int32_t C, int32_t nvec, const float* d_x, float* d_y, void* d_workspace,
+                      size_t workspace_bytes, void* hip_stream) {
+  RungTable rt;
+  const int rc = stream_args(nrows, ncols, C, d_stream, stream_bytes, d_rung_of_block, nrungs,
+                             rungs, d_workspace, workspace_bytes, rt);
+  if (rc != SEEDQ_OK) return rc;
+  if (!(nvec == 1 || nvec == 2 || nvec == 4 || nvec == 8)) return SEEDQ_EINVAL;
+  if (!d_x || !d_y || (reinterpret_cast<uintptr_t>(d_x) & 15u) ||
+      (reinterpret_cast<uintptr_t>(d_y) & 3u))
+    return SEEDQ_EINVAL;
+  const hipError_t e = launch_gemv_stream(d_stream, int64_t(stream_bytes / 4),
+                                          nrungs > 1 ? d_rung_of_block : nullptr, rt, nrows, ncols,
+                                          d_workspace, d_x, ncols, d_y, nrows, nvec,
+                                          static_cast<hipStream_t>(hip_stream));
   return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
 }
 

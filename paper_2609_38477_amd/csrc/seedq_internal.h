@@ -127,7 +127,7 @@ hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const
 // Code stream (seedq_stream.hip). The workspace holds one int64 per chunk of
 // 2048 blocks plus one.
 int64_t stream_chunks(int64_t nblocks);
-size_t stream_workspace_bytes(int64_t nblocks);
+size_t stream_workspace_bytes(int64_t nblocks, int64_t nrows);
 hipError_t launch_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
                        const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
                        uint32_t* d_stream, int64_t nwords, void* d_ws, hipStream_t stream);
@@ -135,6 +135,12 @@ hipError_t launch_pack(const uint32_t* d_seed, const uint8_t* d_exp, const int8_
 hipError_t launch_parse(const uint32_t* d_stream, int64_t nwords, const uint8_t* d_rung,
                         const RungTable& rt, int64_t nblocks, void* d_ws, uint32_t* d_seed,
                         uint8_t* d_exp, int8_t* d_q, float* d_W_hat, hipStream_t stream);
+
+// y_v = W_hat x_v for nv in {1, 2, 4, 8} vectors (x_v = d_x + v * ldx).
+hipError_t launch_gemv_stream(const uint32_t* d_stream, int64_t nwords, const uint8_t* d_rung,
+                              const RungTable& rt, int64_t nrows, int64_t ncols, void* d_ws,
+                              const float* d_x, int64_t ldx, float* d_y, int64_t ldy, int nv,
+                              hipStream_t stream);
 
 // Host planner (seedq_schedule.cpp).
 int derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,

@@ -18,6 +18,8 @@
 // access is coalesced). The packer assembles its chunk in LDS and stores whole
 // words; only the two words a chunk may share with its neighbours are merged
 // with atomic ORs (they are cleared by the offset pass).
+#include <algorithm>
+
 #include "seedq_reconstruct.h"
 
 namespace seedq {
@@ -227,12 +229,108 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
   }
 }
 
+
+// ---------------------------------------------------------------- decode-GEMV
+// y_v = W_hat x_v for nv right-hand sides, W_hat decoded from the stream on the
+// fly and never stored (the bandwidth motivation of the codec: a GEMV reads
+// l(g)/8 bytes per block instead of 16 for fp16). One wave per row: 64 blocks
+// at a time, one per lane, offsets by a wave prefix sum over the rung lengths
+// from the row's start offset; each lane rebuilds its block exactly as
+// seedq_decompress does and accumulates w_hat_i x_v[8g + i] in fp32; a wave
+// reduction gives y_v[r].
+
+__device__ __forceinline__ uint32_t wave_exclusive_scan(uint32_t v, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  *total = __shfl(x, 63, 64);
+  return x - v;
+}
+
+// Bits of every row (one wave per row), then exclusive row offsets.
+__global__ void __launch_bounds__(kThreads)
+row_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
+                int64_t* __restrict__ row_off) {
+  const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+  if (r >= nrows) return;
+  const int lane = threadIdx.x & 63;
+  int64_t sum = 0;
+  for (int64_t g = lane; g < G; g += 64) sum += code_bits(rt, rung ? int(rung[r * G + g]) : 0);
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) sum += __shfl_xor(sum, d, 64);
+  if (lane == 0) row_off[r] = sum;
+}
+
+template <int NV>
+__global__ void __launch_bounds__(kThreads)
+gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
+                   const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
+                   const int64_t* __restrict__ row_off, const float* __restrict__ x,
+                   int64_t ldx, float* __restrict__ y, int64_t ldy) {
+  const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+  if (r >= nrows) return;  // wave-uniform
+  const int lane = threadIdx.x & 63;
+  float acc[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) acc[v] = 0.f;
+  int64_t run = row_off[r];
+  for (int64_t g0 = 0; g0 < G; g0 += 64) {
+    const int64_t g = g0 + lane;
+    const int rr = g < G ? (rung ? int(rung[r * G + g]) : 0) : SEEDQ_MAX_RUNGS;
+    const int len = g < G ? code_bits(rt, rr) : 0;
+    uint32_t tot;
+    const uint32_t ex = wave_exclusive_scan(uint32_t(len), &tot);
+    if (g < G) {
+      const int K = len ? rt.K[rr] : SEEDQ_MIN_K;
+      const int P = len ? rt.P[rr] : 1;
+      uint64_t code = 0;
+      const bool ok = len && read_code(stream, nwords, run + ex, len, code);
+      uint32_t s = 0u;
+      int e = 0;
+      uint2 qw = make_uint2(0u, 0u);
+      if (ok) split_code(code, K, P, s, e, qw);
+      int32_t a[kC];
+      block_acc(ok ? s : 1u, K, P, qw, a);
+      float w[kC];
+      block_weights(a, K, e, ok && s != 0u, w);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const float4* xv = reinterpret_cast<const float4*>(x + v * ldx + g * kC);
+        const float4 x0 = xv[0], x1 = xv[1];
+        float t = acc[v];
+        t = fmaf(w[0], x0.x, t);
+        t = fmaf(w[1], x0.y, t);
+        t = fmaf(w[2], x0.z, t);
+        t = fmaf(w[3], x0.w, t);
+        t = fmaf(w[4], x1.x, t);
+        t = fmaf(w[5], x1.y, t);
+        t = fmaf(w[6], x1.z, t);
+        t = fmaf(w[7], x1.w, t);
+        acc[v] = t;
+      }
+    }
+    run += tot;
+  }
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    float t = acc[v];
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
+    if (lane == 0) y[v * ldy + r] = t;
+  }
+}
+
 }  // namespace
 
 int64_t stream_chunks(int64_t nblocks) { return (nblocks + kChunk - 1) / kChunk; }
 
-size_t stream_workspace_bytes(int64_t nblocks) {
-  return align256(sizeof(int64_t) * size_t(stream_chunks(nblocks) + 1));
+size_t stream_workspace_bytes(int64_t nblocks, int64_t nrows) {
+  const int64_t n = std::max(stream_chunks(nblocks), nrows) + 1;
+  return align256(sizeof(int64_t) * size_t(n));
 }
 
 static hipError_t launch_offsets(const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
@@ -274,6 +372,40 @@ hipError_t launch_parse(const uint32_t* d_stream, int64_t nwords, const uint8_t*
   else
     hipLaunchKernelGGL(parse_kernel<0>, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_stream,
                        nwords, d_rung, rt, nblocks, chunk, d_seed, d_exp, d_q, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_stream(const uint32_t* d_stream, int64_t nwords, const uint8_t* d_rung,
+                              const RungTable& rt, int64_t nrows, int64_t ncols, void* d_ws,
+                              const float* d_x, int64_t ldx, float* d_y, int64_t ldy, int nv,
+                              hipStream_t stream) {
+  int64_t* row_off = static_cast<int64_t*>(d_ws);
+  const int64_t G = ncols / kC;
+  const unsigned grid = unsigned((nrows + kThreads / 64 - 1) / (kThreads / 64));
+  hipLaunchKernelGGL(row_bits_kernel, dim3(grid), dim3(kThreads), 0, stream, d_rung, rt, nrows, G,
+                     row_off);
+  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kThreads), 0, stream, row_off, nrows,
+                     nullptr, int64_t(0));
+  switch (nv) {
+    case 1:
+      hipLaunchKernelGGL(gemv_stream_kernel<1>, dim3(grid), dim3(kThreads), 0, stream, d_stream,
+                         nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
+      break;
+    case 2:
+      hipLaunchKernelGGL(gemv_stream_kernel<2>, dim3(grid), dim3(kThreads), 0, stream, d_stream,
+                         nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
+      break;
+    case 4:
+      hipLaunchKernelGGL(gemv_stream_kernel<4>, dim3(grid), dim3(kThreads), 0, stream, d_stream,
+                         nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
+      break;
+    case 8:
+      hipLaunchKernelGGL(gemv_stream_kernel<8>, dim3(grid), dim3(kThreads), 0, stream, d_stream,
+                         nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

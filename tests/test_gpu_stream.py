@@ -143,3 +143,62 @@ def test_decoder_path_with_rederived_rungs(sq):
     Wd = sq.decompress_stream(words, list(wl.rungs), nrows, wl.ncols, _t(dec_rob))
     Wr, _ = sq.decompress(seed, exp, q, list(wl.rungs), nrows, wl.ncols, _t(rob))
     assert torch.equal(Wd, Wr)
+
+
+def _gemv_bound(W, x):
+    # fp32 accumulation: every lane sums ncols/64 / 8 block partials of 8 fused
+    # products, then a 6-level tree; bound (n_terms_per_lane + 8) u sum |w||x|
+    ncols = W.shape[1]
+    n = (ncols // 8 + 63) // 64 * 8 + 8
+    return n * 2.0 ** -24 * (np.abs(W.astype(np.float64)) @ np.abs(x.astype(np.float64)).T)
+
+
+@pytest.mark.parametrize("nvec", [1, 2, 4, 8])
+def test_gemv_stream_matches_oracle(sq, oq, nvec):
+    import torch
+    nrows, ncols = 37, 8 * 301                 # rows of 301 blocks: 4 lane rounds + a tail
+    nb = nrows * ncols // 8
+    rng = np.random.default_rng(40 + nvec)
+    rob = rng.integers(0, len(MIXED), nb).astype(np.uint8)
+    seed, exp, q = _codes(rng, rob, MIXED)
+    cnt = np.bincount(rob, minlength=len(MIXED))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
+    x = rng.normal(0, 1, (nvec, ncols)).astype(np.float32)
+    y = sq.gemv_stream(w, MIXED, nrows, ncols, _t(x), _t(rob)).cpu().numpy()
+    K_of = np.array([MIXED[r][0] for r in rob])
+    P_of = np.array([MIXED[r][1] for r in rob])
+    Wr, _ = oq.decompress(seed, exp, q, K_of, P_of)
+    Wr = np.asarray(Wr, dtype=np.float32).reshape(nrows, ncols)
+    ref = (Wr.astype(np.float64) @ x.astype(np.float64).T).T
+    assert np.all(np.abs(y - ref) <= _gemv_bound(Wr, x).T + 1e-30)
+
+
+def test_gemv_stream_invalid_block_poisons_its_row(sq):
+    nrows, ncols = 6, 8 * 70
+    nb = nrows * ncols // 8
+    rng = np.random.default_rng(77)
+    rob = rng.integers(0, len(MIXED), nb).astype(np.uint8)
+    rob[3 * 70 + 5] = 7                          # out-of-range rung in row 3
+    seed, exp, q = _codes(rng, rob, MIXED)
+    valid = rob < len(MIXED)
+    cnt = np.bincount(rob[valid], minlength=len(MIXED))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
+    x = rng.normal(0, 1, ncols).astype(np.float32)
+    y = sq.gemv_stream(w, MIXED, nrows, ncols, _t(x), _t(rob)).cpu().numpy()
+    assert np.isnan(y[3]) and not np.isnan(np.delete(y, 3)).any()
+
+
+def test_gemv_stream_full_size(sq):
+    import torch
+    wl = synthetic.WORKLOADS["attn4096"]
+    W = torch.from_numpy(synthetic.workload_weights(wl)).cuda()
+    b = sq.build_bases(16, 3)
+    seed, exp, q, _ = sq.compress(W, [b])
+    w = sq.pack(seed, exp, q, [(16, 3)], wl.nrows, wl.ncols)
+    Wh, _ = sq.decompress(seed, exp, q, [(16, 3)], wl.nrows, wl.ncols)
+    g = torch.Generator(device="cuda").manual_seed(3)
+    x = torch.randn(4, wl.ncols, device="cuda", generator=g)
+    y = sq.gemv_stream(w, [(16, 3)], wl.nrows, wl.ncols, x).cpu().numpy()
+    Wn, xn = Wh.cpu().numpy(), x.cpu().numpy()
+    ref = (Wn.astype(np.float64) @ xn.astype(np.float64).T).T
+    assert np.all(np.abs(y - ref) <= _gemv_bound(Wn, xn).T)
