@@ -113,6 +113,109 @@ def cpu_baseline(W: np.ndarray, K: int, P: int, target_s: float = 15.0) -> dict:
                       f"precomputed outside the timed region"}
 
 
+def decoder_bench(args) -> int:
+    """Decoder path on a searched matrix: host re-derivation of the rungs from
+    the stored lambda / floor / tie count, GPU pack, parse, one-pass decode, and
+    decode-GEMV against a dense GEMV of the decoded weights. Every GPU time is
+    the mean over the timed repetitions of HIP events on the kernels' stream."""
+    import torch
+
+    import paper_2609_38477_amd as sq
+    import synthetic
+
+    wl = synthetic.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    rungs = list(wl.rungs)
+    R = len(rungs)
+    a = synthetic.importance_profile(wl.ncols)
+    log(f"decoder bench on {wl.name}: {wl.note}")
+    W = torch.from_numpy(synthetic.workload_weights(wl)).to(dev)
+    nb = wl.nblocks
+    rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, rungs, wl.damage, wl.target_bpw, a)
+    d_rob = torch.from_numpy(rob).to(dev) if R > 1 else None
+    bases = [sq.build_bases(K, P) for K, P in rungs]
+    seed, exp, q, _ = sq.compress(W, bases, d_rob)
+    counts = rep["count"]
+    nbytes = sq.seedq_stream_bytes(rungs, counts)
+    words = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
+    nws = sq.seedq_stream_workspace_bytes(wl.nrows, wl.ncols)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    s2 = torch.empty_like(seed)
+    e2 = torch.empty_like(exp)
+    q2 = torch.empty_like(q)
+    W_hat = torch.empty_like(W)
+    g = torch.Generator(device="cuda").manual_seed(0)
+    xs = {nv: torch.randn(nv, wl.ncols, device=dev, generator=g) for nv in (1, 4, 8)}
+    ys = {nv: torch.empty(nv, wl.nrows, device=dev) for nv in (1, 4, 8)}
+    rung_arg = d_rob if R > 1 else None
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(reps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    reps = max(args.steps, 5) * 4
+    t0 = time.perf_counter()
+    for _ in range(3):
+        dec_rob = sq.derive_schedule(wl.nrows, wl.ncols, rungs, wl.damage, a, rep["lam"],
+                                     rep["floor_q"], rep["tie_count"])
+    derive_ms = (time.perf_counter() - t0) / 3 * 1e3
+    assert np.array_equal(dec_rob, rob)
+    ms = {}
+    ms["pack"] = timed(lambda: sq.seedq_pack(seed, exp, q, rung_arg, rungs, wl.nrows, wl.ncols, 8,
+                                             words, nbytes, ws, nws, stream), reps)
+    ms["unpack"] = timed(lambda: sq.seedq_unpack(words, nbytes, rung_arg, rungs, wl.nrows, wl.ncols,
+                                                 8, s2, e2, q2, ws, nws, stream), reps)
+    ms["decompress_stream"] = timed(lambda: sq.seedq_decompress_stream(
+        words, nbytes, rung_arg, rungs, wl.nrows, wl.ncols, 8, W_hat, ws, nws, stream), reps)
+    ms["decompress_codes"] = timed(lambda: sq.seedq_decompress(
+        seed, exp, q, rung_arg, rungs, wl.nrows, wl.ncols, 8, W_hat, None, stream), reps)
+    for nv in (1, 4, 8):
+        ms[f"gemv_stream_x{nv}"] = timed(lambda nv=nv: sq.seedq_gemv_stream(
+            words, nbytes, rung_arg, rungs, wl.nrows, wl.ncols, 8, nv, xs[nv], ys[nv], ws, nws,
+            stream), reps)
+    # dense references on the decoded weights (vendor GEMV/GEMM, context only)
+    W16 = W_hat.half()
+    x16 = {nv: xs[nv].half() for nv in (1, 4, 8)}
+    for nv in (1, 4, 8):
+        ms[f"dense_fp16_x{nv}"] = timed(lambda nv=nv: torch.matmul(W16, x16[nv].t()), reps)
+        ms[f"dense_fp32_x{nv}"] = timed(lambda nv=nv: torch.matmul(W_hat, xs[nv].t()), reps)
+    assert torch.equal(s2, seed) and torch.equal(e2, exp)
+
+    stream_b = nbytes
+    rung_b = nb if R > 1 else 0
+    hbm = {  # algorithmic HBM bytes per launch
+        "pack": nb * (4 + 1 + 8) + rung_b + stream_b,
+        "unpack": stream_b + rung_b + nb * (4 + 1 + 8),
+        "decompress_stream": stream_b + rung_b + nb * 32,
+        "decompress_codes": nb * (4 + 1 + 8) + rung_b + nb * 32,
+    }
+    for nv in (1, 4, 8):
+        hbm[f"gemv_stream_x{nv}"] = stream_b + rung_b + 4 * nv * (wl.ncols + wl.nrows)
+        hbm[f"dense_fp16_x{nv}"] = 2 * wl.nrows * wl.ncols + 2 * nv * (wl.ncols + wl.nrows)
+        hbm[f"dense_fp32_x{nv}"] = 4 * wl.nrows * wl.ncols + 4 * nv * (wl.ncols + wl.nrows)
+    kernels = {k: {"ms": v, "hbm_bytes": hbm[k], "GBps": hbm[k] / (v / 1e3) / 1e9,
+                   "hbm_frac": hbm[k] / (v / 1e3) / 1e9 / PEAK_HBM_GBS} for k, v in ms.items()}
+    out = {"metric": "decoder path: decoded weights/s and HBM GB/s per kernel; 1 GPU",
+           "workload": wl.name, "shape": [wl.nrows, wl.ncols], "nblocks": nb,
+           "rungs": [list(r) for r in rungs], "target_bpw": wl.target_bpw,
+           "payload_bytes": nbytes, "payload_bits_per_weight": 8.0 * nbytes / (8 * nb),
+           "derive_schedule_host_ms": derive_ms, "kernels": kernels,
+           "decoded_weights_per_s": {k: 8 * nb / (v / 1e3) for k, v in ms.items()
+                                     if k.startswith(("decompress", "gemv"))},
+           "data": "synthetic"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,6 +225,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-gemm-reference", action="store_true")
+    ap.add_argument("--decoder", action="store_true",
+                    help="time the decoder path (derive, pack, parse, decode, decode-GEMV) instead")
     ap.add_argument("--gemm-reference-only", action="store_true",
                     help="only time the fp16 GEMM used as the practical matrix-core reference")
     args = ap.parse_args()
@@ -142,6 +247,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.decoder:
+        return decoder_bench(args)
     wl = synthetic.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)

@@ -106,6 +106,10 @@ def lib() -> ctypes.CDLL:
         L.seedq_gemv_stream.restype = ctypes.c_int
         L.seedq_gemv_stream.argtypes = [vp, sz, vp, i32, ctypes.POINTER(Rung), i64, i64, i32, i32,
                                         vp, vp, vp, sz, vp]
+        L.seedq_footprint_workspace_bytes.restype = sz
+        L.seedq_footprint_workspace_bytes.argtypes = []
+        L.seedq_footprint.restype = ctypes.c_int
+        L.seedq_footprint.argtypes = [vp, vp, i64, vp, vp, vp, sz, vp]
         _lib = L
     return _lib
 
@@ -235,6 +239,17 @@ def seedq_gemv_stream(d_stream, stream_bytes: int, d_rung_of_block, rungs, nrows
                                  _rungs(rungs), nrows, ncols, C, nvec, _ptr(d_x), _ptr(d_y),
                                  _ptr(d_workspace), workspace_bytes, _stream(stream))
     _check(rc, "seedq_gemv_stream")
+
+
+def seedq_footprint_workspace_bytes() -> int:
+    return int(lib().seedq_footprint_workspace_bytes())
+
+
+def seedq_footprint(d_clean, d_corrupt, n: int, d_count, d_sums, d_workspace, workspace_bytes: int,
+                    stream=None) -> None:
+    rc = lib().seedq_footprint(_ptr(d_clean), _ptr(d_corrupt), n, _ptr(d_count), _ptr(d_sums),
+                               _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_footprint")
 
 
 # ---------------------------------------------------------------- helpers
@@ -396,3 +411,17 @@ def gemv_stream(words, rungs, nrows: int, ncols: int, x, rung_of_block=None, str
     seedq_gemv_stream(words, words.numel() * 4, rung_of_block, rungs, nrows, ncols, SEEDQ_BLOCK,
                       xx.shape[0], xx, y, ws, nws, stream)
     return y[0] if squeeze else y
+
+
+def footprint(clean, corrupt, stream=None):
+    """(N_flip, p_flip, eta) of eq. (security_metrics) for two fp32 GPU tensors."""
+    import torch
+    n = clean.numel()
+    cnt = torch.zeros(1, dtype=torch.int64, device=clean.device)
+    sums = torch.zeros(2, dtype=torch.float64, device=clean.device)
+    nws = seedq_footprint_workspace_bytes()
+    ws = torch.empty(nws, dtype=torch.uint8, device=clean.device)
+    seedq_footprint(clean.contiguous(), corrupt.contiguous(), n, cnt, sums, ws, nws, stream)
+    c = int(cnt.item())
+    s = sums.cpu().numpy()
+    return c, c / n, float(np.sqrt(s[0] / s[1])) if s[1] > 0 else float("nan")

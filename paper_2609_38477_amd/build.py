@@ -14,7 +14,8 @@ LIB_NAME = "libseedq.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 HIP_SOURCES = ["seedq_bases.hip", "seedq_search.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
-               "seedq_decompress.hip", "seedq_stream.hip"]
+               "seedq_decompress.hip", "seedq_stream.hip",
+               "seedq_footprint.hip"]
 HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp"]
 
 # Device code is compiled without packed fp32 instructions.

@@ -246,4 +246,20 @@ int seedq_gemv_stream(const uint32_t* d_stream, size_t stream_bytes, const uint8
   return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
 }
 
+size_t seedq_footprint_workspace_bytes(void) { return footprint_workspace_bytes(); }
+
+int seedq_footprint(const float* d_clean, const float* d_corrupt, int64_t n, long long* d_count,
+                    double* d_sums, void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+  if (!d_clean || !d_corrupt || !d_count || !d_sums || n < 0) return SEEDQ_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(d_clean) & 15u) || (reinterpret_cast<uintptr_t>(d_corrupt) & 15u) ||
+      (reinterpret_cast<uintptr_t>(d_count) & 7u) || (reinterpret_cast<uintptr_t>(d_sums) & 7u))
+    return SEEDQ_EINVAL;
+  if (!d_workspace || workspace_bytes < footprint_workspace_bytes() ||
+      (reinterpret_cast<uintptr_t>(d_workspace) & 255u))
+    return SEEDQ_EWORKSPACE;
+  const hipError_t e = launch_footprint(d_clean, d_corrupt, n, d_workspace, d_count, d_sums,
+                                        static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
 }  // extern "C"

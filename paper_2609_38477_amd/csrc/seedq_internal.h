@@ -142,6 +142,12 @@ hipError_t launch_gemv_stream(const uint32_t* d_stream, int64_t nwords, const ui
                               const float* d_x, int64_t ldx, float* d_y, int64_t ldy, int nv,
                               hipStream_t stream);
 
+// Fault footprint (seedq_footprint.hip): *d_count = N_flip, d_sums = {sum of
+// squared differences, sum of squared clean weights}.
+size_t footprint_workspace_bytes();
+hipError_t launch_footprint(const float* d_clean, const float* d_corrupt, int64_t n, void* d_ws,
+                            long long* d_count, double* d_sums, hipStream_t stream);
+
 // Host planner (seedq_schedule.cpp).
 int derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,
                     int64_t tie_count, uint8_t* rung_of_block);

@@ -60,17 +60,33 @@ __device__ uint32_t wg_exclusive_scan(uint32_t v, uint32_t* total) {
   return before + x - v;
 }
 
+// Lengths of 8 consecutive blocks from their rung bytes (8-byte loads where
+// the chunk is whole, byte loads at the ragged end).
+__device__ __forceinline__ uint32_t bits_of_8(const uint8_t* __restrict__ rung, const RungTable& rt,
+                                              int64_t b0, int64_t nblocks) {
+  if (!rung) {
+    const int64_t n = min(int64_t(8), nblocks - b0);
+    return n > 0 ? uint32_t(n) * uint32_t(code_bits(rt, 0)) : 0u;
+  }
+  uint32_t sum = 0;
+  if (b0 + 8 <= nblocks && (reinterpret_cast<uintptr_t>(rung + b0) & 7u) == 0) {
+    const uint2 v = *reinterpret_cast<const uint2*>(rung + b0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sum += code_bits(rt, int((v.x >> (8 * i)) & 0xFFu));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sum += code_bits(rt, int((v.y >> (8 * i)) & 0xFFu));
+  } else {
+    for (int64_t b = b0; b < min(b0 + 8, nblocks); ++b) sum += code_bits(rt, int(rung[b]));
+  }
+  return sum;
+}
+
 __global__ void __launch_bounds__(kThreads)
 chunk_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nblocks,
                   int64_t* __restrict__ chunk) {
-  const int64_t base = int64_t(blockIdx.x) * kChunk;
-  uint32_t sum = 0;
-  for (int it = 0; it < kIters; ++it) {
-    const int64_t b = base + it * kThreads + threadIdx.x;
-    if (b < nblocks) sum += code_bits(rt, rung ? int(rung[b]) : 0);
-  }
+  const int64_t b0 = int64_t(blockIdx.x) * kChunk + int64_t(threadIdx.x) * kIters;
   uint32_t tot;
-  wg_exclusive_scan(sum, &tot);
+  wg_exclusive_scan(bits_of_8(rung, rt, b0, nblocks), &tot);
   if (threadIdx.x == 0) chunk[blockIdx.x] = tot;
 }
 
@@ -80,32 +96,37 @@ chunk_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nblock
 __global__ void __launch_bounds__(kThreads)
 chunk_offsets_kernel(int64_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ stream,
                      int64_t nwords) {
-  __shared__ int64_t part[kThreads];
+  __shared__ int64_t part[kThreads / 64];
   const int64_t per = (nchunks + kThreads - 1) / kThreads;
   const int64_t c0 = min(nchunks, int64_t(threadIdx.x) * per);
   const int64_t c1 = min(nchunks, c0 + per);
   int64_t s = 0;
   for (int64_t c = c0; c < c1; ++c) s += chunk[c];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int64_t run = 0;
-    for (int t = 0; t < kThreads; ++t) {
-      const int64_t v = part[t];
-      part[t] = run;
-      run += v;
-    }
-    chunk[nchunks] = run;
+  // exclusive scan of the per-thread sums: within each wave by shuffles, then
+  // across the four waves
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int64_t x = s;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
   }
+  if (lane == 63) part[wave] = x;
   __syncthreads();
-  int64_t run = part[threadIdx.x];
+  int64_t run = x - s, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) {
+    run += w < wave ? part[w] : 0;
+    tot += part[w];
+  }
+  if (threadIdx.x == 0) chunk[nchunks] = tot;
   for (int64_t c = c0; c < c1; ++c) {
     const int64_t v = chunk[c];
     chunk[c] = run;
     if (stream && (run >> 5) < nwords) stream[run >> 5] = 0u;
     run += v;
   }
-  if (stream && threadIdx.x == 0 && (chunk[nchunks] >> 5) < nwords) stream[chunk[nchunks] >> 5] = 0u;
+  if (stream && threadIdx.x == 0 && (tot >> 5) < nwords) stream[tot >> 5] = 0u;
 }
 
 __global__ void __launch_bounds__(kThreads)
@@ -259,7 +280,8 @@ row_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, i
   if (r >= nrows) return;
   const int lane = threadIdx.x & 63;
   int64_t sum = 0;
-  for (int64_t g = lane; g < G; g += 64) sum += code_bits(rt, rung ? int(rung[r * G + g]) : 0);
+  const uint8_t* row = rung ? rung + r * G : nullptr;
+  for (int64_t g = 8 * lane; g < G; g += 8 * 64) sum += bits_of_8(row, rt, g, G);
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) sum += __shfl_xor(sum, d, 64);
   if (lane == 0) row_off[r] = sum;

@@ -1,0 +1,55 @@
+"""GPU footprint kernel against the oracle's eq. (security_metrics), and the
+single-bit fault study through the decoder path.
+
+Bars: N_flip exact; eta to 1e-12 relative (fp64 sums in another order); a
+payload fault changes weights of its own block only; every table fault is
+caught by the table checksum."""
+import numpy as np
+import pytest
+
+import synthetic
+from oracle import stream as ostream
+
+pytestmark = pytest.mark.gpu
+
+
+def test_footprint_kernel_matches_oracle():
+    import torch
+    import paper_2609_38477_amd as sq
+    rng = np.random.default_rng(8)
+    for n in (1, 7, 4096 * 4 + 3, 3_000_001):
+        a = rng.normal(0, 1, n).astype(np.float32)
+        b = a.copy()
+        k = rng.choice(n, size=min(n, 37), replace=False)
+        b[k] += rng.normal(0, 1, k.size).astype(np.float32)
+        got = sq.footprint(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda())
+        ref = ostream.footprint(a, b)
+        assert got[0] == ref[0] and got[1] == ref[1]
+        assert abs(got[2] - ref[2]) <= 1e-12 * max(ref[2], 1e-300)
+    b[5] = np.nan                                   # a NaN difference counts as changed
+    got = sq.footprint(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda())
+    assert got[0] == ostream.footprint(a, b)[0] and np.isnan(got[2])
+
+
+def test_fault_study_payload_faults_stay_in_their_block():
+    import torch
+    from paper_2609_38477_amd import faults
+    wl = synthetic.WORKLOADS["reduced"]
+    W = synthetic.weights(64, wl.ncols, wl.sigma, 21, wl.outlier_frac)
+    enc = faults.Encoded(torch.from_numpy(W).cuda(), wl.rungs, wl.damage, 3.296875,
+                         synthetic.importance_profile(wl.ncols))
+    assert enc.rep["tie_count"] > 0
+    clean = enc.decode().cpu().numpy().reshape(-1, 8)
+    b = 20000
+    o = int(enc.block_offset[b])
+    K = enc.rungs[int(enc.rob[b])][0]
+    for n in (o, o + K - 1, o + K, o + K + 7):
+        bad = enc.decode(enc.flip_stream_bit(n)).cpu().numpy().reshape(-1, 8)
+        changed = np.nonzero(np.any(bad != clean, axis=1))[0]
+        assert changed.tolist() == [b], n
+    rows = faults.study(enc, block=b)
+    payload = [r for r in rows if "block" in r["fault"]]
+    table = [r for r in rows if "block" not in r["fault"]]
+    assert len(payload) == 4 and all(0 < r["N_flip"] <= 8 for r in payload)
+    assert table and all(r["table_checksum_detects"] for r in table)
+    assert any(r.get("N_flip", 0) > 1000 for r in table)
