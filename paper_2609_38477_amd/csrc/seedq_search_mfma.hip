@@ -30,7 +30,10 @@
 // Block tiles go to the matrix core in pairs (six products) before the vector
 // ALU folds them, with one branch per pair; the fold waits on its own
 // products, so it is occupancy (several waves per SIMD) that keeps the matrix
-// core busy.
+// core busy. For P >= 4 the fp64 evaluation needs more registers than the
+// walk leaves free, so a second kernel rebuilds the block data and reloads the
+// seed-tile fragments after every evaluation batch instead of keeping them
+// live across it, and runs at four waves per SIMD.
 #include <cmath>
 #include <type_traits>
 
@@ -47,6 +50,7 @@ constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
 constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
+constexpr int kPilotTiles = 1;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
 // Row and column of pair k (i <= j, row-major over the upper triangle) for
@@ -178,6 +182,277 @@ static_assert(kSlots <= 128, "slot must fit 7 bits");
 template <int P>
 __global__ void __launch_bounds__(kWaves * 64)
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
+                   const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
+                   const double* __restrict__ pinv64, const half8* __restrict__ pi16,
+                   int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
+                   uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
+                   float* __restrict__ err_out) {
+  __shared__ unsigned long long keys_all[kWaves][kSlots];
+  __shared__ int32_t blk_all[kWaves][kSlots];
+  __shared__ uint32_t queue_all[kWaves][kQCap];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n = lane & 31;   // block column of the MFMA tile
+  const int h = lane >> 5;   // which half of the rows / reduction this lane holds
+  unsigned long long* keys = keys_all[wave];
+  int32_t* blk = blk_all[wave];
+  uint32_t* queue = queue_all[wave];
+
+  int64_t begin = 0, count = nblocks;
+  if (list) {
+    begin = off[rung];
+    count = int64_t(off[rung + 1]) - begin;
+  }
+  const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
+  if (wave_base >= count) return;  // wave-uniform; waves never synchronise
+  const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
+
+  // ---------------------------------------------------------------- prologue
+  half8 bop[kNB][3];
+  float thr[kNB], thr_base[kNB];
+  int ex[kNB];
+  bool active[kNB], valid[kNB];
+#pragma unroll
+  for (int nt = 0; nt < kNB; ++nt) {
+    const int64_t idx = wave_base + nt * 32 + n;
+    valid[nt] = idx < count;
+    const int64_t b = valid[nt] ? (list ? int64_t(list[begin + idx]) : idx) : 0;
+    float w[kC];
+    load_block(W, b, valid[nt], w);
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
+    active[nt] = valid[nt] && amax > 0.f;
+    ex[nt] = active[nt] ? ilogbf(amax) : 0;
+    float ws[kC], ww = 0.f;
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      ws[i] = ldexpf(w[i], -ex[nt]);
+      ww = fmaf(ws[i], ws[i], ww);
+    }
+    // thresholds live in accumulator units (both operands carry 2^12)
+    thr_base[nt] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+    thr[nt] = active[nt] ? -INFINITY : INFINITY;
+    bop[nt][0] = b_fragment<0>(ws, h);
+    bop[nt][1] = b_fragment<1>(ws, h);
+    bop[nt][2] = b_fragment<2>(ws, h);
+    if (h == 0) {
+      keys[nt * 32 + n] = ~0ull;
+      blk[nt * 32 + n] = int32_t(b);
+    }
+  }
+  __threadfence_block();
+
+  int qcount = 0;  // wave-uniform
+  // Evaluate the top min(64, qcount) entries, one per lane, until fewer than
+  // min_batch remain; then rebuild the screening thresholds from the keys.
+  auto flush = [&](int min_batch) __attribute__((always_inline)) {
+    __threadfence_block();
+    while (qcount >= min_batch && qcount > 0) {
+      const int e = qcount < 64 ? qcount : 64;
+      const int base = qcount - e;
+      if (lane < e) {
+        const uint32_t ent = queue[base + lane];
+        const uint32_t seed = ent >> 8;
+        const int slot = int(ent & 0x7Fu);
+        if (seed != 0u) {
+          const int64_t b = blk[slot];
+          float w[kC];
+          load_block(W, b, true, w);
+          int qe, q[P];
+          const double err =
+              exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          if (ent & kFinal) {
+            seed_out[b] = seed;
+            exp_out[b] = uint8_t(qe);
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+              const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
+              if (p < 4) lo |= byte << (8 * p);
+              else hi |= byte << (8 * (p - 4));
+            }
+            reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
+            if (err_out) err_out[b] = float(err);
+          } else {
+            atomicMin(&keys[slot], (unsigned long long)candidate_key(err, seed));
+          }
+        }
+      }
+      qcount = base;
+    }
+    __threadfence_block();
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const unsigned long long key = keys[nt * 32 + n];
+      if (active[nt] && key != ~0ull) {
+        const double bound = key_error(key) * (1.0 + 0x1p-27);
+        thr[nt] = thr_base[nt] - __double2float_ru(ldexp(bound, 24 - 2 * ex[nt]));
+      }
+    }
+  };
+
+  const half8* A = pi16;
+
+  // ---------------------------------------------------------------- pilot
+  // Over the first tile(s) each lane tracks its seed of smallest bound; their
+  // exact errors start every block's best. (Longer pilots cost more matrix
+  // time than the survivors they save.)
+  {
+    const int64_t npilot = ntiles < kPilotTiles ? ntiles : kPilotTiles;
+    float pm[kNB];
+    uint32_t ps[kNB];
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      pm[nt] = -INFINITY;
+      ps[nt] = 0u;
+    }
+    for (int64_t T = 0; T < npilot; ++T) {
+      const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
+      const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+#pragma unroll
+      for (int nt = 0; nt < kNB; ++nt) {
+        const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+        const float m = fold_max(acc);
+        if (m > pm[nt]) {
+          int jb = 15;
+#pragma unroll
+          for (int j = 14; j >= 0; --j)
+            if (acc[j] == m) jb = j;
+          const uint32_t sd = seed_of(seedbase, jb, h);
+          if (sd <= nseeds) {
+            pm[nt] = m;
+            ps[nt] = sd;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const bool put = active[nt] && ps[nt] != 0u;
+      const uint64_t mk = ballot(put);
+      if (put) queue[qcount + lanes_below(mk)] = (ps[nt] << 8) | uint32_t(nt * 32 + n);
+      qcount += __popcll(mk);
+    }
+    flush(1);
+  }
+
+  // ---------------------------------------------------------------- seed walk
+  // Queue the candidates of block tile nt whose bound passes. At most 1024 per
+  // block tile; fewer than 64 are queued before a pair of block tiles, so the
+  // 2 x 1024 of one pair always fit.
+  auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
+                   __attribute__((always_inline)) {
+    constexpr int nt = decltype(ntc)::value;
+    if (ballot(any) != 0ull) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool pass = acc[j] >= thr[nt];
+        const uint64_t mk = ballot(pass);
+        if (mk != 0ull) {
+          if (pass) {
+            const uint32_t seed = seed_of(seedbase, j, h);
+            queue[qcount + lanes_below(mk)] =
+                ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
+          }
+          qcount += __popcll(mk);
+        }
+      }
+    }
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  static_assert(kNB == 4, "the walk below unrolls four block tiles");
+
+  // One seed tile against the four block tiles: two block tiles at a time,
+  // six products to the matrix core, then the folds, one branch per pair.
+  auto tile = [&](const half8& a0, const half8& a1, const half8& a2, int64_t T)
+                  __attribute__((always_inline)) {
+    const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+    {
+      const floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
+      const floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
+      const bool p0 = fold_max(acc0) >= thr[0];
+      const bool p1 = fold_max(acc1) >= thr[1];
+      if ((ballot(p0) | ballot(p1)) != 0ull) {
+        check(I0{}, acc0, p0, seedbase);
+        check(I1{}, acc1, p1, seedbase);
+        if (qcount >= 64) flush(64);
+      }
+    }
+    {
+      const floatx16 acc2 = bounds(a0, a1, a2, bop[2]);
+      const floatx16 acc3 = bounds(a0, a1, a2, bop[3]);
+      const bool p2 = fold_max(acc2) >= thr[2];
+      const bool p3 = fold_max(acc3) >= thr[3];
+      if ((ballot(p2) | ballot(p3)) != 0ull) {
+        check(I2{}, acc2, p2, seedbase);
+        check(I3{}, acc3, p3, seedbase);
+        if (qcount >= 64) flush(64);
+      }
+    }
+  };
+  // Two register sets of seed-tile fragments in turn: the set of one tile is
+  // loaded while the other tile is screened. The loads are unconditional (the
+  // index is clamped to the last tile) so that the wait before each tile
+  // covers only that tile's own loads.
+  const int64_t last = ntiles - 1;
+  half8 x0 = A[lane], x1 = A[64 + lane], x2 = A[128 + lane];
+  half8 y0, y1, y2;
+  for (int64_t T = 0; T < ntiles; T += 2) {
+    {
+      const half8* An = A + (T + 1 < last ? T + 1 : last) * 192;
+      y0 = An[lane];
+      y1 = An[64 + lane];
+      y2 = An[128 + lane];
+    }
+    tile(x0, x1, x2, T);
+    {
+      const half8* An = A + (T + 2 < last ? T + 2 : last) * 192;
+      x0 = An[lane];
+      x1 = An[64 + lane];
+      x2 = An[128 + lane];
+    }
+    if (T + 1 < ntiles) tile(y0, y1, y2, T + 1);
+  }
+  flush(1);
+
+  // ---------------------------------------------------------------- results
+  // the winning seed of every block, evaluated once more to emit its code
+#pragma unroll
+  for (int nt = 0; nt < kNB; ++nt) {
+    const bool put = h == 0 && active[nt];
+    const uint64_t mk = ballot(put);
+    if (put) {
+      const unsigned long long key = keys[nt * 32 + n];
+      // every active block has a key after the pilot; seed 1 is a guard
+      const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
+      queue[qcount + lanes_below(mk)] = (seed << 8) | kFinal | uint32_t(nt * 32 + n);
+    }
+    qcount += __popcll(mk);
+    if (h == 0 && valid[nt] && !active[nt]) {
+      // all-zero block: every seed ties, the smallest one wins
+      const int64_t b = blk[nt * 32 + n];
+      seed_out[b] = 1u;
+      exp_out[b] = 15;
+      reinterpret_cast<uint2*>(q_out)[b] = make_uint2(0u, 0u);
+      if (err_out) err_out[b] = 0.f;
+    }
+  }
+  flush(1);
+}
+
+// The same search for P >= 4, where the fp64 evaluation needs more registers:
+// the block data (B fragments and thresholds) and the seed-tile fragments are
+// rebuilt from W, the keys and the projector stack after every evaluation
+// batch, so none of it is live across that code and the kernel fits four waves
+// per SIMD.
+template <int P>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
+search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
@@ -460,9 +735,14 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.exp_out = d_exp;
   a.q_out = d_q;
   a.err_out = d_err;
-  hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
-                     a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16, a.ntiles,
-                     a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
+  if constexpr (P >= 4)
+    hipLaunchKernelGGL(search_mfma_remat_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0,
+                       stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
+                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
+  else
+    hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
+                       a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
+                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
   return hipGetLastError();
 }
 
