@@ -110,6 +110,29 @@ def lib() -> ctypes.CDLL:
         L.seedq_footprint_workspace_bytes.argtypes = []
         L.seedq_footprint.restype = ctypes.c_int
         L.seedq_footprint.argtypes = [vp, vp, i64, vp, vp, vp, sz, vp]
+        dp = ctypes.POINTER(ctypes.c_double)
+        L.seedq_gauss_hermite.restype = ctypes.c_int
+        L.seedq_gauss_hermite.argtypes = [i32, vp, vp]
+        L.seedq_sq_gemv_workspace_bytes.restype = sz
+        L.seedq_sq_gemv_workspace_bytes.argtypes = [i64, i64, i32]
+        L.seedq_sq_gemv.restype = ctypes.c_int
+        L.seedq_sq_gemv.argtypes = [vp, i64, i64, vp, i32, vp, vp, sz, vp]
+        L.seedq_column_stats.restype = ctypes.c_int
+        L.seedq_column_stats.argtypes = [vp, i64, i64, vp, vp, vp]
+        L.seedq_expect_silu_sq.restype = ctypes.c_int
+        L.seedq_expect_silu_sq.argtypes = [vp, i64, i32, vp, vp]
+        L.seedq_channel_order.restype = ctypes.c_int
+        L.seedq_channel_order.argtypes = [vp, i64, vp]
+        L.seedq_permute_columns.restype = ctypes.c_int
+        L.seedq_permute_columns.argtypes = [vp, i64, i64, vp, i32, vp, vp]
+        L.seedq_select_outliers.restype = ctypes.c_int
+        L.seedq_select_outliers.argtypes = [i32, vp, ctypes.POINTER(dp), ctypes.POINTER(dp),
+                                            ctypes.POINTER(dp), i32, vp, vp,
+                                            ctypes.POINTER(ctypes.c_int32)]
+        L.seedq_extract_columns.restype = ctypes.c_int
+        L.seedq_extract_columns.argtypes = [vp, i64, i64, i32, vp, vp, vp]
+        L.seedq_apply_columns.restype = ctypes.c_int
+        L.seedq_apply_columns.argtypes = [vp, i64, i64, i32, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -250,6 +273,77 @@ def seedq_footprint(d_clean, d_corrupt, n: int, d_count, d_sums, d_workspace, wo
     rc = lib().seedq_footprint(_ptr(d_clean), _ptr(d_corrupt), n, _ptr(d_count), _ptr(d_sums),
                                _ptr(d_workspace), workspace_bytes, _stream(stream))
     _check(rc, "seedq_footprint")
+
+
+def seedq_gauss_hermite(n: int):
+    x = np.empty(n, dtype=np.float64)
+    w = np.empty(n, dtype=np.float64)
+    _check(lib().seedq_gauss_hermite(n, x.ctypes.data, w.ctypes.data), "seedq_gauss_hermite")
+    return x, w
+
+
+def seedq_sq_gemv_workspace_bytes(nrows: int, ncols: int, transpose: int) -> int:
+    return int(lib().seedq_sq_gemv_workspace_bytes(nrows, ncols, int(transpose)))
+
+
+def seedq_sq_gemv(d_W, nrows: int, ncols: int, d_v, transpose: int, d_out, d_workspace=None,
+                  workspace_bytes: int = 0, stream=None) -> None:
+    rc = lib().seedq_sq_gemv(_ptr(d_W), nrows, ncols, _ptr(d_v), int(transpose), _ptr(d_out),
+                             _ptr(d_workspace), workspace_bytes, _stream(stream))
+    _check(rc, "seedq_sq_gemv")
+
+
+def seedq_column_stats(d_W, nrows: int, ncols: int, d_maxabs, d_median, stream=None) -> None:
+    _check(lib().seedq_column_stats(_ptr(d_W), nrows, ncols, _ptr(d_maxabs), _ptr(d_median),
+                                    _stream(stream)), "seedq_column_stats")
+
+
+def seedq_expect_silu_sq(d_var, n: int, nodes: int, d_out, stream=None) -> None:
+    _check(lib().seedq_expect_silu_sq(_ptr(d_var), n, nodes, _ptr(d_out), _stream(stream)),
+           "seedq_expect_silu_sq")
+
+
+def seedq_channel_order(a) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    perm = np.empty(a.size, dtype=np.int32)
+    _check(lib().seedq_channel_order(a.ctypes.data, a.size, perm.ctypes.data), "seedq_channel_order")
+    return perm
+
+
+def seedq_permute_columns(d_in, nrows: int, ncols: int, d_perm, inverse: int, d_out,
+                          stream=None) -> None:
+    _check(lib().seedq_permute_columns(_ptr(d_in), nrows, ncols, _ptr(d_perm), int(inverse),
+                                       _ptr(d_out), _stream(stream)), "seedq_permute_columns")
+
+
+def seedq_select_outliers(maxabs_list, median_list, a_list, keep: int = 4):
+    """[(tensor, column)] of the kept outlier columns (host numpy fp64 inputs)."""
+    T = len(maxabs_list)
+    mx = [np.ascontiguousarray(m, dtype=np.float64) for m in maxabs_list]
+    md = [np.ascontiguousarray(m, dtype=np.float64) for m in median_list]
+    aa = [np.ascontiguousarray(m, dtype=np.float64) for m in a_list]
+    ncols = np.array([m.size for m in mx], dtype=np.int64)
+    dp = ctypes.POINTER(ctypes.c_double)
+    arr = lambda lst: (dp * max(T, 1))(*[m.ctypes.data_as(dp) for m in lst])
+    ot = np.empty(max(keep, 1), dtype=np.int32)
+    oc = np.empty(max(keep, 1), dtype=np.int32)
+    cnt = ctypes.c_int32(0)
+    rc = lib().seedq_select_outliers(T, ncols.ctypes.data, arr(mx), arr(md), arr(aa), keep,
+                                     ot.ctypes.data, oc.ctypes.data, ctypes.byref(cnt))
+    _check(rc, "seedq_select_outliers")
+    return [(int(ot[i]), int(oc[i])) for i in range(cnt.value)]
+
+
+def seedq_extract_columns(d_W, nrows: int, ncols: int, ncol: int, d_cols, d_fp16,
+                          stream=None) -> None:
+    _check(lib().seedq_extract_columns(_ptr(d_W), nrows, ncols, ncol, _ptr(d_cols), _ptr(d_fp16),
+                                       _stream(stream)), "seedq_extract_columns")
+
+
+def seedq_apply_columns(d_W, nrows: int, ncols: int, ncol: int, d_cols, d_fp16,
+                        stream=None) -> None:
+    _check(lib().seedq_apply_columns(_ptr(d_W), nrows, ncols, ncol, _ptr(d_cols), _ptr(d_fp16),
+                                     _stream(stream)), "seedq_apply_columns")
 
 
 # ---------------------------------------------------------------- helpers

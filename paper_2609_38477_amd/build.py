@@ -15,8 +15,8 @@ LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 HIP_SOURCES = ["seedq_bases.hip", "seedq_search.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
                "seedq_decompress.hip", "seedq_stream.hip",
-               "seedq_footprint.hip"]
-HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp"]
+               "seedq_footprint.hip", "seedq_frontend.hip"]
+HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp", "seedq_frontend_host.cpp"]
 
 # Device code is compiled without packed fp32 instructions.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

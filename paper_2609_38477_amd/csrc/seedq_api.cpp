@@ -262,4 +262,88 @@ int seedq_footprint(const float* d_clean, const float* d_corrupt, int64_t n, lon
   return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
 }
 
+int seedq_gauss_hermite(int32_t n, double* x, double* w) { return gauss_hermite(n, x, w); }
+
+size_t seedq_sq_gemv_workspace_bytes(int64_t nrows, int64_t ncols, int32_t transpose) {
+  if (nrows <= 0 || ncols <= 0) return 0;
+  return sq_gemv_workspace_bytes(nrows, ncols, transpose ? 1 : 0);
+}
+
+int seedq_sq_gemv(const float* d_W, int64_t nrows, int64_t ncols, const float* d_v,
+                  int32_t transpose, double* d_out, void* d_workspace, size_t workspace_bytes,
+                  void* hip_stream) {
+  if (!d_W || !d_v || !d_out || nrows <= 0 || ncols <= 0) return SEEDQ_EINVAL;
+  if (!transpose && ((ncols & 3) || (reinterpret_cast<uintptr_t>(d_W) & 15u) ||
+                     (reinterpret_cast<uintptr_t>(d_v) & 15u)))
+    return SEEDQ_EINVAL;
+  const size_t need = sq_gemv_workspace_bytes(nrows, ncols, transpose ? 1 : 0);
+  if (need && (!d_workspace || workspace_bytes < need ||
+               (reinterpret_cast<uintptr_t>(d_workspace) & 255u)))
+    return SEEDQ_EWORKSPACE;
+  const hipError_t e = launch_sq_gemv(d_W, nrows, ncols, d_v, transpose ? 1 : 0, d_out, d_workspace,
+                                      static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_column_stats(const float* d_W, int64_t nrows, int64_t ncols, double* d_maxabs,
+                       double* d_median, void* hip_stream) {
+  if (!d_W || !d_maxabs || !d_median || nrows <= 0 || ncols <= 0) return SEEDQ_EINVAL;
+  const hipError_t e = launch_column_stats(d_W, nrows, ncols, d_maxabs, d_median,
+                                           static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_expect_silu_sq(const double* d_var, int64_t n, int32_t nodes, double* d_out,
+                         void* hip_stream) {
+  if (!d_var || !d_out || n < 0 || nodes < 1 || nodes > 128) return SEEDQ_EINVAL;
+  if (n == 0) return SEEDQ_OK;
+  double x[128], w[128];
+  const int rc = gauss_hermite(nodes, x, w);
+  if (rc != SEEDQ_OK) return rc;
+  const hipError_t e =
+      launch_expect_silu_sq(d_var, n, nodes, x, w, d_out, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_channel_order(const float* a, int64_t n, int32_t* perm) {
+  if (!a || !perm || n < 0 || n > (int64_t(1) << 31) - 1) return SEEDQ_EINVAL;
+  channel_order(a, n, perm);
+  return SEEDQ_OK;
+}
+
+int seedq_permute_columns(const float* d_in, int64_t nrows, int64_t ncols, const int32_t* d_perm,
+                          int32_t inverse, float* d_out, void* hip_stream) {
+  if (!d_in || !d_out || !d_perm || nrows <= 0 || ncols <= 0 || d_in == d_out) return SEEDQ_EINVAL;
+  const hipError_t e = launch_permute_columns(d_in, nrows, ncols, d_perm, inverse ? 1 : 0, d_out,
+                                              static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_select_outliers(int32_t ntensors, const int64_t* ncols, const double* const* maxabs,
+                          const double* const* median, const double* const* a, int32_t keep,
+                          int32_t* out_tensor, int32_t* out_col, int32_t* out_count) {
+  return select_outliers(ntensors, ncols, maxabs, median, a, keep, out_tensor, out_col, out_count);
+}
+
+int seedq_extract_columns(const float* d_W, int64_t nrows, int64_t ncols, int32_t ncol,
+                          const int32_t* d_cols, void* d_fp16, void* hip_stream) {
+  if (!d_W || nrows <= 0 || ncols <= 0 || ncol < 0 || ncol > 65535) return SEEDQ_EINVAL;
+  if (ncol == 0) return SEEDQ_OK;
+  if (!d_cols || !d_fp16) return SEEDQ_EINVAL;
+  const hipError_t e = launch_columns_fp16(const_cast<float*>(d_W), nrows, ncols, ncol, d_cols,
+                                           d_fp16, 0, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_apply_columns(float* d_W, int64_t nrows, int64_t ncols, int32_t ncol,
+                        const int32_t* d_cols, const void* d_fp16, void* hip_stream) {
+  if (!d_W || nrows <= 0 || ncols <= 0 || ncol < 0 || ncol > 65535) return SEEDQ_EINVAL;
+  if (ncol == 0) return SEEDQ_OK;
+  if (!d_cols || !d_fp16) return SEEDQ_EINVAL;
+  const hipError_t e = launch_columns_fp16(d_W, nrows, ncols, ncol, d_cols,
+                                           const_cast<void*>(d_fp16), 1,
+                                           static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
 }  // extern "C"

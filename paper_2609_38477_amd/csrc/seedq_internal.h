@@ -148,6 +148,25 @@ size_t footprint_workspace_bytes();
 hipError_t launch_footprint(const float* d_clean, const float* d_corrupt, int64_t n, void* d_ws,
                             long long* d_count, double* d_sums, hipStream_t stream);
 
+// Importance front end (seedq_frontend.hip, seedq_frontend_host.cpp).
+size_t sq_gemv_workspace_bytes(int64_t nrows, int64_t ncols, int transpose);
+hipError_t launch_sq_gemv(const float* d_W, int64_t nrows, int64_t ncols, const float* d_v,
+                          int transpose, double* d_out, void* d_ws, hipStream_t stream);
+hipError_t launch_column_stats(const float* d_W, int64_t nrows, int64_t ncols, double* d_max,
+                               double* d_median, hipStream_t stream);
+hipError_t launch_expect_silu_sq(const double* d_var, int64_t n, int nodes, const double* x,
+                                 const double* w, double* d_out, hipStream_t stream);
+hipError_t launch_permute_columns(const float* d_in, int64_t nrows, int64_t ncols,
+                                  const int32_t* d_perm, int inverse, float* d_out,
+                                  hipStream_t stream);
+hipError_t launch_columns_fp16(float* d_W, int64_t nrows, int64_t ncols, int32_t ncol,
+                               const int32_t* d_cols, void* d_f16, int apply, hipStream_t stream);
+int gauss_hermite(int n, double* x, double* w);
+void channel_order(const float* a, int64_t n, int32_t* perm);
+int select_outliers(int32_t ntensors, const int64_t* ncols, const double* const* maxabs,
+                    const double* const* median, const double* const* a, int32_t keep,
+                    int32_t* out_tensor, int32_t* out_col, int32_t* out_count);
+
 // Host planner (seedq_schedule.cpp).
 int derive_schedule(const seedq_schedule_desc* desc, double lambda, double floor_q,
                     int64_t tie_count, uint8_t* rung_of_block);

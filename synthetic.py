@@ -191,3 +191,39 @@ WORKLOADS = {
 
 def workload_weights(wl: Workload) -> np.ndarray:
     return weights(wl.nrows, wl.ncols, wl.sigma, wl.key, wl.outlier_frac)
+
+
+@dataclass
+class SyntheticLayer:
+    """One pre-norm transformer layer plus a language-model head, random weights
+    (no checkpoint is read): RMSNorm gains around 1 with one massive-activation
+    channel, projection weights N(0, sigma^2) with the workloads' outliers, and
+    one planted super weight in W_down."""
+    d: int
+    f: int
+    n_heads: int
+    n_kv_heads: int
+    vocab: int
+    tensors: dict = field(default_factory=dict)   # name -> fp32 [out, in]
+    gains: dict = field(default_factory=dict)     # "attn", "mlp" -> fp32 [d]
+    super_weight: tuple = (0, 0)                  # (row, column) in W_down
+    massive_channel: int = 0                      # channel of gains["mlp"]
+
+
+def synthetic_layer(d: int = 512, f: int = 1536, n_heads: int = 8, n_kv_heads: int = 2,
+                    vocab: int = 2048, key: int = 9, sigma: float = 0.02) -> SyntheticLayer:
+    hd = d // n_heads
+    L = SyntheticLayer(d, f, n_heads, n_kv_heads, vocab)
+    shapes = {"q": (d, d), "k": (n_kv_heads * hd, d), "v": (n_kv_heads * hd, d), "o": (d, d),
+              "gate": (f, d), "up": (f, d), "down": (d, f), "lm_head": (vocab, d)}
+    for i, (name, (r, c)) in enumerate(shapes.items()):
+        L.tensors[name] = weights(r, c, sigma, key * 16 + i, 0.001)
+    for i, name in enumerate(("attn", "mlp")):
+        z = normal(key * 16 + 10 + i, STREAM_MISC, d)
+        L.gains[name] = np.exp(0.3 * z).astype(np.float32)
+    u = splitmix64(key, STREAM_MISC, 3, start=1 << 20)
+    L.massive_channel = int(u[0] % np.uint64(d))
+    L.gains["mlp"][L.massive_channel] = 30.0
+    L.super_weight = (int(u[1] % np.uint64(d)), int(u[2] % np.uint64(f)))
+    L.tensors["down"][L.super_weight] = 20.0
+    return L
