@@ -14,23 +14,26 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
                                              int (&q)[P]) {
 #pragma clang fp contract(off)
   double t[P];
+  int e = 15;
 #pragma unroll
   for (int p = 0; p < P; ++p) {
     double acc = 0.0;
 #pragma unroll
     for (int i = 0; i < kC; ++i) acc = acc + A[p * kC + i] * double(w[i]);
     t[p] = acc;
-  }
-  // largest e in [0, 15] at which every rne(t_p 2^e) lies in [-8, 7]
-  int e = 15;
-  for (; e >= 0; --e) {
-    bool fits = true;
-#pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const double r = rint(ldexp(t[p], e));
-      fits = fits && (r <= 7.0) && (r >= -8.0);
+    // The largest e in [0, 15] at which every rne(t_p 2^e) lies in [-8, 7], in
+    // closed form, folded into the coefficient loop. A positive t = f 2^E
+    // (f in [0.5, 1)) fits while t 2^e < 7.5: up to e = 3 - E when f < 15/16,
+    // else 2 - E. A negative one fits while |t| 2^e <= 8.5 (rne(-8.5) = -8):
+    // up to e = 4 - E when f <= 17/32, else 3 - E. Fitting is monotone in e, so
+    // the answer is the smallest limit and 15; below 0 no scale fits and e = 0
+    // with clamping.
+    if (acc != 0.0) {
+      const double f = __builtin_amdgcn_frexp_mant(acc < 0.0 ? -acc : acc);
+      const int E = __builtin_amdgcn_frexp_exp(acc);
+      const int lim = acc > 0.0 ? (f < 0.9375 ? 3 - E : 2 - E) : (f <= 0.53125 ? 4 - E : 3 - E);
+      e = lim < e ? lim : e;
     }
-    if (fits) break;
   }
   if (e < 0) e = 0;
 #pragma unroll

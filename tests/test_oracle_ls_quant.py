@@ -107,3 +107,34 @@ def test_quantiser_c_matches_numpy(oq):
     for i in range(len(t)):
         e, q = oq.quantize(t[i])
         assert e == e2[i] and np.array_equal(q, q2[i])
+
+
+def test_closed_form_exponent_equals_the_exponent_search(oq):
+    # The kernels pick the shared exponent in closed form from frexp of every
+    # coefficient; the definition (R6) searches e from 15 down. Check the two
+    # agree at every boundary the closed form uses (mantissas 7.5 and -8.5
+    # times 2^-e, one ulp either side) and on random coefficients.
+    import math
+    import numpy as np
+
+    def closed(t):
+        e = 15
+        for v in t:
+            if v != 0.0:
+                f, E = math.frexp(abs(v))
+                lim = (3 - E if f < 0.9375 else 2 - E) if v > 0 else (4 - E if f <= 0.53125 else 3 - E)
+                e = min(e, lim)
+        return max(e, 0)
+
+    vals = []
+    for e in range(-3, 18):
+        for base in (7.5, -8.5, 7.0, -8.0, 3.75, -4.25):
+            x = math.ldexp(base, -e)
+            vals += [x, np.nextafter(x, np.inf), np.nextafter(x, -np.inf)]
+    rng = np.random.default_rng(0)
+    cases = [np.array([v, 0.0, 0.0]) for v in vals]
+    cases += [rng.normal(0, 10.0 ** rng.uniform(-4, 1), 3) for _ in range(3000)]
+    cases += [np.zeros(3)]
+    for t in cases:
+        e_ref, _ = oq.quantize(np.asarray(t, dtype=np.float64))
+        assert closed(t) == e_ref, t
