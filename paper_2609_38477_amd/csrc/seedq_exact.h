@@ -41,6 +41,8 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
     const double r = fmin(fmax(rint(ldexp(t[p], e)), -8.0), 7.0);
     q[p] = int(r);
   }
+  // x - 2^(K-1) lies in [-2^23, 2^23) for K <= 24, so each product is one
+  // signed 24-bit multiply-add.
   const int32_t half = int32_t(1) << (K - 1);
   int32_t acc[kC];
 #pragma unroll
@@ -50,7 +52,7 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
   for (int j = 0; j < P; ++j) {
 #pragma unroll
     for (int i = 0; i < kC; ++i) {
-      acc[i] += (int32_t(x) - half) * q[j];
+      acc[i] += __mul24(int32_t(x) - half, q[j]);
       x = lfsr_step(x, mask);
     }
   }

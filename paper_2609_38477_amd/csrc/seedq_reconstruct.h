@@ -9,19 +9,38 @@
 namespace seedq {
 
 // q_j is the signed byte j of qw (bytes 0-3 in qw.x, 4-7 in qw.y).
+// acc_i = sum_j (x_{8j+i} - 2^(K-1)) q_j is formed as sum_j x q_j - 2^(K-1) sum_j q_j:
+// for K <= 23 every state fits a signed 24-bit operand, so each product is one
+// full-rate 24-bit multiply-add (|x q| < 2^26, every partial sum < 2^29).
 __device__ __forceinline__ void block_acc(uint32_t s, int K, int P, uint2 qw, int32_t (&acc)[kC]) {
   const uint32_t mask = lfsr_mask(K);
   const int32_t half = int32_t(1) << (K - 1);
 #pragma unroll
   for (int i = 0; i < kC; ++i) acc[i] = 0;
   uint32_t x = s;
-  for (int j = 0; j < P; ++j) {
-    const uint32_t word = (j < 4) ? qw.x : qw.y;
-    const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+  if (K <= 23) {
+    int32_t qsum = 0;
+    for (int j = 0; j < P; ++j) {
+      const uint32_t word = (j < 4) ? qw.x : qw.y;
+      const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+      qsum += qj;
 #pragma unroll
-    for (int i = 0; i < kC; ++i) {
-      acc[i] += (int32_t(x) - half) * qj;
-      x = lfsr_step(x, mask);
+      for (int i = 0; i < kC; ++i) {
+        acc[i] += __mul24(int32_t(x), qj);
+        x = lfsr_step(x, mask);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kC; ++i) acc[i] -= half * qsum;
+  } else {
+    for (int j = 0; j < P; ++j) {
+      const uint32_t word = (j < 4) ? qw.x : qw.y;
+      const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+#pragma unroll
+      for (int i = 0; i < kC; ++i) {
+        acc[i] += __mul24(int32_t(x) - half, qj);   // x - 2^23 fits 24 bits
+        x = lfsr_step(x, mask);
+      }
     }
   }
 }
