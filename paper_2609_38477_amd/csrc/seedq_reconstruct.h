@@ -8,21 +8,26 @@
 
 namespace seedq {
 
-// q_j is the signed byte j of qw (bytes 0-3 in qw.x, 4-7 in qw.y).
-// acc_i = sum_j (x_{8j+i} - 2^(K-1)) q_j is formed as sum_j x q_j - 2^(K-1) sum_j q_j:
-// for K <= 23 every state fits a signed 24-bit operand, so each product is one
-// full-rate 24-bit multiply-add (|x q| < 2^26, every partial sum < 2^29).
-__device__ __forceinline__ void block_acc(uint32_t s, int K, int P, uint2 qw, int32_t (&acc)[kC]) {
-  const uint32_t mask = lfsr_mask(K);
+// acc_i = sum_j (x_{8j+i} - 2^(K-1)) q_j, with q_j = qat(j) in [-8, 7], P >= 1
+// and the LFSR feedback mask of K. It is formed as sum_j x q_j - 2^(K-1)
+// sum_j q_j: for K <= 23 every state fits a signed 24-bit operand, so each
+// product is one full-rate 24-bit multiply-add (|x q| < 2^26, every partial
+// sum < 2^29). The first coefficient is peeled so that acc needs no clearing.
+template <typename QAt>
+__device__ __forceinline__ void block_acc_q(uint32_t s, int K, int P, uint32_t mask, QAt qat,
+                                            int32_t (&acc)[kC]) {
   const int32_t half = int32_t(1) << (K - 1);
-#pragma unroll
-  for (int i = 0; i < kC; ++i) acc[i] = 0;
   uint32_t x = s;
-  if (K <= 23) {
-    int32_t qsum = 0;
-    for (int j = 0; j < P; ++j) {
-      const uint32_t word = (j < 4) ? qw.x : qw.y;
-      const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+  if (__builtin_expect(K <= 23, 1)) {
+    const int32_t q0 = qat(0);
+    int32_t qsum = q0;
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      acc[i] = __mul24(int32_t(x), q0);
+      x = lfsr_step(x, mask);
+    }
+    for (int j = 1; j < P; ++j) {
+      const int32_t qj = qat(j);
       qsum += qj;
 #pragma unroll
       for (int i = 0; i < kC; ++i) {
@@ -30,19 +35,33 @@ __device__ __forceinline__ void block_acc(uint32_t s, int K, int P, uint2 qw, in
         x = lfsr_step(x, mask);
       }
     }
+    const int32_t c = half * qsum;
 #pragma unroll
-    for (int i = 0; i < kC; ++i) acc[i] -= half * qsum;
+    for (int i = 0; i < kC; ++i) acc[i] -= c;
   } else {
-    for (int j = 0; j < P; ++j) {
-      const uint32_t word = (j < 4) ? qw.x : qw.y;
-      const int32_t qj = int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+    const int32_t q0 = qat(0);
+#pragma unroll
+    for (int i = 0; i < kC; ++i) {
+      acc[i] = __mul24(int32_t(x) - half, q0);   // x - 2^23 fits 24 bits
+      x = lfsr_step(x, mask);
+    }
+    for (int j = 1; j < P; ++j) {
+      const int32_t qj = qat(j);
 #pragma unroll
       for (int i = 0; i < kC; ++i) {
-        acc[i] += __mul24(int32_t(x) - half, qj);   // x - 2^23 fits 24 bits
+        acc[i] += __mul24(int32_t(x) - half, qj);
         x = lfsr_step(x, mask);
       }
     }
   }
+}
+
+// q_j is the signed byte j of qw (bytes 0-3 in qw.x, 4-7 in qw.y).
+__device__ __forceinline__ void block_acc(uint32_t s, int K, int P, uint2 qw, int32_t (&acc)[kC]) {
+  block_acc_q(s, K, P, lfsr_mask(K), [&](int j) {
+    const uint32_t word = (j < 4) ? qw.x : qw.y;
+    return int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+  }, acc);
 }
 
 // w_hat_i = acc_i 2^-(K-1+e), NaN for an invalid code.

@@ -254,11 +254,17 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
 // ---------------------------------------------------------------- decode-GEMV
 // y_v = W_hat x_v for nv right-hand sides, W_hat decoded from the stream on the
 // fly and never stored (the bandwidth motivation of the codec: a GEMV reads
-// l(g)/8 bytes per block instead of 16 for fp16). One wave per row: 64 blocks
-// at a time, one per lane, offsets by a wave prefix sum over the rung lengths
-// from the row's start offset; each lane rebuilds its block exactly as
-// seedq_decompress does and accumulates w_hat_i x_v[8g + i] in fp32; a wave
-// reduction gives y_v[r].
+// l(g)/8 bytes per block instead of 16 for fp16). One wave per row, 256 blocks
+// per wave step as 4 sub-steps of 64 consecutive blocks, one per lane, so the
+// loads of x stay coalesced. The offsets of all four sub-steps come from one
+// wave prefix sum over 64-bit words holding the four bit counts in 16-bit
+// fields (a sub-step holds at most 64 x 52 bits). A block's code is read as
+// one 64-bit window (two funnel shifts of three words); its rung constants (K,
+// P, feedback mask, length) come from a table in LDS. The lane rebuilds the
+// block's integers exactly as seedq_decompress does and forms
+// d_v = sum_i fp32(acc_i) x_v[8g + i]; since w_hat_i = fp32(acc_i) 2^-(K-1+e)
+// exactly, d_v 2^-(K-1+e) is the block's partial product up to fp32 rounding.
+// A wave reduction gives y_v[r].
 
 __device__ __forceinline__ uint32_t wave_exclusive_scan(uint32_t v, uint32_t* total) {
   const int lane = threadIdx.x & 63;
@@ -266,6 +272,18 @@ __device__ __forceinline__ uint32_t wave_exclusive_scan(uint32_t v, uint32_t* to
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
     const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  *total = __shfl(x, 63, 64);
+  return x - v;
+}
+
+__device__ __forceinline__ uint64_t wave_exclusive_scan64(uint64_t v, uint64_t* total) {
+  const int lane = threadIdx.x & 63;
+  uint64_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t y = __shfl_up(x, d, 64);
     if (lane >= d) x += y;
   }
   *total = __shfl(x, 63, 64);
@@ -287,55 +305,105 @@ row_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, i
   if (lane == 0) row_off[r] = sum;
 }
 
+constexpr int kGemvNB = 4;  // sub-steps of 64 blocks per wave step
+
 template <int NV>
 __global__ void __launch_bounds__(kThreads)
 gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
                    const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
                    const int64_t* __restrict__ row_off, const float* __restrict__ x,
                    int64_t ldx, float* __restrict__ y, int64_t ldy) {
+  // (K, P, feedback mask, code length) per rung; entry rt.n (and every rung
+  // byte >= rt.n, clamped to it) is an invalid code of length 0.
+  __shared__ uint4 tab[SEEDQ_MAX_RUNGS + 1];
+  if (threadIdx.x <= SEEDQ_MAX_RUNGS) {
+    const int t = int(threadIdx.x);
+    const bool v = t < rt.n;
+    const int K = v ? rt.K[t] : SEEDQ_MIN_K;
+    const int P = v ? rt.P[t] : 1;
+    tab[t] = make_uint4(uint32_t(K), uint32_t(P), lfsr_mask(K), v ? uint32_t(K + 4 + 4 * P) : 0u);
+  }
+  __syncthreads();
   const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
   if (r >= nrows) return;  // wave-uniform
   const int lane = threadIdx.x & 63;
+  const int64_t nbits = nwords << 5;
+  const int64_t last = nwords - 1;
+  const uint32_t nr = uint32_t(rt.n);
   float acc[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) acc[v] = 0.f;
+  const uint8_t* row = rung ? rung + r * G : nullptr;
   int64_t run = row_off[r];
-  for (int64_t g0 = 0; g0 < G; g0 += 64) {
-    const int64_t g = g0 + lane;
-    const int rr = g < G ? (rung ? int(rung[r * G + g]) : 0) : SEEDQ_MAX_RUNGS;
-    const int len = g < G ? code_bits(rt, rr) : 0;
-    uint32_t tot;
-    const uint32_t ex = wave_exclusive_scan(uint32_t(len), &tot);
-    if (g < G) {
-      const int K = len ? rt.K[rr] : SEEDQ_MIN_K;
-      const int P = len ? rt.P[rr] : 1;
-      uint64_t code = 0;
-      const bool ok = len && read_code(stream, nwords, run + ex, len, code);
-      uint32_t s = 0u;
-      int e = 0;
-      uint2 qw = make_uint2(0u, 0u);
-      if (ok) split_code(code, K, P, s, e, qw);
-      int32_t a[kC];
-      block_acc(ok ? s : 1u, K, P, qw, a);
-      float w[kC];
-      block_weights(a, K, e, ok && s != 0u, w);
+  for (int64_t g0 = 0; g0 < G; g0 += 64 * kGemvNB) {
+    uint4 info[kGemvNB];
+    uint64_t lbits = 0u;  // bit counts of the lane's blocks, 16 bits per sub-step
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const float4* xv = reinterpret_cast<const float4*>(x + v * ldx + g * kC);
-        const float4 x0 = xv[0], x1 = xv[1];
-        float t = acc[v];
-        t = fmaf(w[0], x0.x, t);
-        t = fmaf(w[1], x0.y, t);
-        t = fmaf(w[2], x0.z, t);
-        t = fmaf(w[3], x0.w, t);
-        t = fmaf(w[4], x1.x, t);
-        t = fmaf(w[5], x1.y, t);
-        t = fmaf(w[6], x1.z, t);
-        t = fmaf(w[7], x1.w, t);
-        acc[v] = t;
+    for (int k = 0; k < kGemvNB; ++k) {
+      const int64_t g = g0 + 64 * k + lane;
+      const uint32_t rr = g < G ? (row ? uint32_t(row[g]) : 0u) : nr;
+      info[k] = tab[rr < nr ? rr : nr];
+      if (g >= G) info[k].w = 0u;
+      lbits |= uint64_t(info[k].w) << (16 * k);
+    }
+    uint64_t tot;
+    const uint64_t ex = wave_exclusive_scan64(lbits, &tot);
+#pragma unroll
+    for (int k = 0; k < kGemvNB; ++k) {
+      const int64_t g = g0 + 64 * k + lane;
+      const int64_t pos = run + int64_t((ex >> (16 * k)) & 0xFFFFu);
+      run += int64_t((tot >> (16 * k)) & 0xFFFFu);
+      if (g < G) {
+        const int K = int(info[k].x), P = int(info[k].y);
+        const uint32_t len = info[k].w;
+        bool ok = len != 0u && pos + int64_t(len) <= nbits;
+        uint32_t lo = 0u, hi = 0u;
+        if (ok) {
+          const int64_t wi = pos >> 5;
+          const uint32_t* sp = stream + wi;
+          uint32_t a, b, c;
+          if (wi + 2 <= last) {
+            a = sp[0];
+            b = sp[1];
+            c = sp[2];
+          } else {  // the last two words of the stream
+            a = sp[0];
+            b = wi + 1 <= last ? sp[1] : 0u;
+            c = 0u;
+          }
+          // bits at and above len belong to the next block (or are zero past
+          // the stream's end); no field below reads them
+          const uint32_t sh = uint32_t(pos) & 31u;
+          lo = __builtin_amdgcn_alignbit(b, a, sh);
+          hi = __builtin_amdgcn_alignbit(c, b, sh);
+        }
+        const uint32_t s = lo & ((1u << K) - 1u);
+        const int e = int((lo >> K) & 15u);
+        const uint32_t qb = __builtin_amdgcn_alignbit(hi, lo, uint32_t(K + 4));
+        ok = ok && s != 0u;
+        int32_t a8[kC];
+        block_acc_q(ok ? s : 1u, K, P, info[k].z,
+                    [&](int j) { return __builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4); }, a8);
+        float f[kC];
+#pragma unroll
+        for (int i = 0; i < kC; ++i) f[i] = __int2float_rn(a8[i]);
+        const int sc = -(K - 1 + e);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const float4* xv = reinterpret_cast<const float4*>(x + v * ldx + g * kC);
+          const float4 x0 = xv[0], x1 = xv[1];
+          float d = f[0] * x0.x;
+          d = fmaf(f[1], x0.y, d);
+          d = fmaf(f[2], x0.z, d);
+          d = fmaf(f[3], x0.w, d);
+          d = fmaf(f[4], x1.x, d);
+          d = fmaf(f[5], x1.y, d);
+          d = fmaf(f[6], x1.z, d);
+          d = fmaf(f[7], x1.w, d);
+          acc[v] += ok ? ldexpf(d, sc) : __int_as_float(0x7fc00000);
+        }
       }
     }
-    run += tot;
   }
 #pragma unroll
   for (int v = 0; v < NV; ++v) {

@@ -146,8 +146,9 @@ def test_decoder_path_with_rederived_rungs(sq):
 
 
 def _gemv_bound(W, x):
-    # fp32 accumulation: every lane sums ncols/64 / 8 block partials of 8 fused
-    # products, then a 6-level tree; bound (n_terms_per_lane + 8) u sum |w||x|
+    # fp32 accumulation: every lane adds at most 4 ceil(G / 256) block partials
+    # (G = ncols / 8), each a chain of 8 fused products, then a 6-level tree; the
+    # bound used, (8 ceil(G / 64) + 8) u sum |w||x|, is above that term count
     ncols = W.shape[1]
     n = (ncols // 8 + 63) // 64 * 8 + 8
     return n * 2.0 ** -24 * (np.abs(W.astype(np.float64)) @ np.abs(x.astype(np.float64)).T)
