@@ -15,18 +15,25 @@ __global__ void __launch_bounds__(256)
 decompress_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
                   const int8_t* __restrict__ q, const uint8_t* __restrict__ rung, RungTable rt,
                   int64_t nblocks, float* __restrict__ W_hat, int32_t* __restrict__ acc_out) {
+  // rung constants from LDS keep the per-lane lookup off the memory path, so
+  // a block's loads all issue at once
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
+  __syncthreads();
   const int64_t b = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (b >= nblocks) return;
-  const int r = rung ? int(rung[b]) : 0;
-  bool ok = r < rt.n;
-  const int K = ok ? rt.K[r] : SEEDQ_MIN_K;
-  const int P = ok ? rt.P[r] : 1;
+  const uint32_t r = rung ? uint32_t(rung[b]) : 0u;
   const uint32_t s = seed[b];
   const int e = expo[b];
-  ok = ok && s >= 1u && s < (1u << K) && e <= 15;
   const uint2 qw = reinterpret_cast<const uint2*>(q)[b];
+  const uint4 in = tab[table_index(r, uint32_t(rt.n))];
+  const int K = int(in.x), P = int(in.y);
+  const bool ok = in.w != 0u && s >= 1u && s < (1u << K) && e <= 15;
   int32_t acc[kC];
-  block_acc(s, K, P, qw, acc);
+  block_acc_q(s, K, P, in.z, [&](int j) {
+    const uint32_t word = (j < 4) ? qw.x : qw.y;
+    return int32_t(int8_t(uint8_t(word >> (8 * (j & 3)))));
+  }, acc);
   float o[kC];
   block_weights(acc, K, e, ok, o);
   if (!ok) {

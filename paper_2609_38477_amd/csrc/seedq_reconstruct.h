@@ -8,6 +8,25 @@
 
 namespace seedq {
 
+// Rung constants for per-lane lookups, kept in LDS: entry r = (K, P, LFSR
+// feedback mask, code length l = K + 4 + 4P) of rung r < n, and entry n (n =
+// rt.n <= SEEDQ_MAX_RUNGS) stands for every rung byte >= n: an invalid code of
+// length 0 (K = SEEDQ_MIN_K, P = 1 keep its arithmetic in range). Threads
+// 0..SEEDQ_MAX_RUNGS fill it; the caller synchronises before reading.
+constexpr int kRungTable = SEEDQ_MAX_RUNGS + 1;
+
+__device__ __forceinline__ void fill_rung_table(uint4* tab, const RungTable& rt) {
+  if (threadIdx.x < kRungTable) {
+    const int t = int(threadIdx.x);
+    const bool v = t < rt.n;
+    const int K = v ? rt.K[t] : SEEDQ_MIN_K;
+    const int P = v ? rt.P[t] : 1;
+    tab[t] = make_uint4(uint32_t(K), uint32_t(P), lfsr_mask(K), v ? uint32_t(K + 4 + 4 * P) : 0u);
+  }
+}
+
+__device__ __forceinline__ uint32_t table_index(uint32_t r, uint32_t n) { return r < n ? r : n; }
+
 // acc_i = sum_j (x_{8j+i} - 2^(K-1)) q_j, with q_j = qat(j) in [-8, 7], P >= 1
 // and the LFSR feedback mask of K. It is formed as sum_j x q_j - 2^(K-1)
 // sum_j q_j: for K <= 23 every state fits a signed 24-bit operand, so each

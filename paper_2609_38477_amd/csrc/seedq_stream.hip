@@ -13,11 +13,13 @@
 // Every kernel walks the blocks in chunks of 2048 (one workgroup each): a first
 // pass sums the lengths of every chunk, one workgroup turns the sums into the
 // bit offset of every chunk, and the chunk's workgroup then finds each block's
-// offset with workgroup prefix sums over its rung lengths (256 blocks at a
-// time, so neighbouring threads handle neighbouring blocks and every global
-// access is coalesced). The packer assembles its chunk in LDS and stores whole
-// words; only the two words a chunk may share with its neighbours are merged
-// with atomic ORs (they are cleared by the offset pass).
+// offset with one workgroup prefix sum over the rung lengths of all its eight
+// 256-block iterations at once (eight 16-bit fields in two 64-bit words), so
+// neighbouring threads handle neighbouring blocks, every global access is
+// coalesced and a chunk needs two barriers. Rung constants come from a small
+// table in LDS. The packer assembles its chunk in LDS and stores whole words;
+// only the two words a chunk may share with its neighbours are merged with
+// atomic ORs (they are cleared by the offset pass).
 #include <algorithm>
 
 #include "seedq_reconstruct.h"
@@ -32,62 +34,111 @@ constexpr int kMaxBlockBits = SEEDQ_MAX_K + 4 + 4 * SEEDQ_MAX_P;
 // bit 31 + every bit of a chunk, plus the two words a code may spill into
 constexpr int kStageWords = (31 + kChunk * kMaxBlockBits) / 32 + 3;
 
-__device__ __forceinline__ int code_bits(const RungTable& rt, int r) {
-  return r < rt.n ? rt.K[r] + 4 + 4 * rt.P[r] : 0;
-}
-
-// Exclusive prefix sum of v over the workgroup; *total receives the sum.
-__device__ uint32_t wg_exclusive_scan(uint32_t v, uint32_t* total) {
-  __shared__ uint32_t wsum[kThreads / 64];
+// Exclusive prefix sums over the workgroup of eight 16-bit fields at once
+// (fields 0-3 in v.x, 4-7 in v.y, field k in bits 16(k mod 4) and up). Every
+// field's workgroup total stays below 2^16 (kThreads codes of at most
+// kMaxBlockBits bits), so the 64-bit sums never carry from one field into the
+// next. *total receives the workgroup totals.
+static_assert(kThreads * kMaxBlockBits < 65536, "a 16-bit field holds one iteration's bits");
+__device__ ulonglong2 wg_exclusive_scan8(ulonglong2 v, ulonglong2* total) {
+  __shared__ unsigned long long wsum[2][kThreads / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
+  unsigned long long a = v.x, b = v.y;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
+    const unsigned long long ya = __shfl_up(a, d, 64), yb = __shfl_up(b, d, 64);
+    if (lane >= d) {
+      a += ya;
+      b += yb;
+    }
   }
-  if (lane == 63) wsum[wave] = x;
+  if (lane == 63) {
+    wsum[0][wave] = a;
+    wsum[1][wave] = b;
+  }
   __syncthreads();
-  uint32_t before = 0, tot = 0;
+  unsigned long long ba = 0, bb = 0, ta = 0, tb = 0;
 #pragma unroll
   for (int w = 0; w < kThreads / 64; ++w) {
-    const uint32_t s = wsum[w];
-    before += (w < wave) ? s : 0u;
-    tot += s;
+    const unsigned long long sa = wsum[0][w], sb = wsum[1][w];
+    ba += (w < wave) ? sa : 0ull;
+    bb += (w < wave) ? sb : 0ull;
+    ta += sa;
+    tb += sb;
   }
   __syncthreads();
-  *total = tot;
-  return before + x - v;
+  *total = make_ulonglong2(ta, tb);
+  return make_ulonglong2(ba + a - v.x, bb + b - v.y);
+}
+
+__device__ __forceinline__ uint32_t field16(ulonglong2 v, int k) {
+  return uint32_t(((k < 4 ? v.x : v.y) >> (16 * (k & 3))) & 0xFFFFu);
 }
 
 // Lengths of 8 consecutive blocks from their rung bytes (8-byte loads where
-// the chunk is whole, byte loads at the ragged end).
-__device__ __forceinline__ uint32_t bits_of_8(const uint8_t* __restrict__ rung, const RungTable& rt,
-                                              int64_t b0, int64_t nblocks) {
+// the run is whole and aligned, byte loads at a ragged end).
+__device__ __forceinline__ uint32_t bits_of_8(const uint8_t* __restrict__ rung, const uint4* tab,
+                                              uint32_t nr, int64_t b0, int64_t nblocks) {
   if (!rung) {
     const int64_t n = min(int64_t(8), nblocks - b0);
-    return n > 0 ? uint32_t(n) * uint32_t(code_bits(rt, 0)) : 0u;
+    return n > 0 ? uint32_t(n) * tab[0].w : 0u;
   }
   uint32_t sum = 0;
   if (b0 + 8 <= nblocks && (reinterpret_cast<uintptr_t>(rung + b0) & 7u) == 0) {
     const uint2 v = *reinterpret_cast<const uint2*>(rung + b0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sum += code_bits(rt, int((v.x >> (8 * i)) & 0xFFu));
+    for (int i = 0; i < 4; ++i) sum += tab[table_index((v.x >> (8 * i)) & 0xFFu, nr)].w;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sum += code_bits(rt, int((v.y >> (8 * i)) & 0xFFu));
+    for (int i = 0; i < 4; ++i) sum += tab[table_index((v.y >> (8 * i)) & 0xFFu, nr)].w;
   } else {
-    for (int64_t b = b0; b < min(b0 + 8, nblocks); ++b) sum += code_bits(rt, int(rung[b]));
+    for (int64_t b = b0; b < min(b0 + 8, nblocks); ++b) sum += tab[table_index(rung[b], nr)].w;
   }
   return sum;
+}
+
+// The 64 stream bits from bit pos on, as (lo, hi); false when the len bits at
+// pos are not all inside the stream (then lo and hi are untouched). Bits past
+// len belong to the next block, or are zero past the stream's end.
+__device__ __forceinline__ bool read_window(const uint32_t* __restrict__ stream, int64_t nwords,
+                                            int64_t pos, uint32_t len, uint32_t& lo, uint32_t& hi) {
+  if (len == 0u || pos + int64_t(len) > (nwords << 5)) return false;
+  const int64_t wi = pos >> 5;
+  const uint32_t* sp = stream + wi;
+  uint32_t a, b, c;
+  if (wi + 2 < nwords) {
+    a = sp[0];
+    b = sp[1];
+    c = sp[2];
+  } else {
+    a = sp[0];
+    b = wi + 1 < nwords ? sp[1] : 0u;
+    c = 0u;
+  }
+  const uint32_t sh = uint32_t(pos) & 31u;
+  lo = __builtin_amdgcn_alignbit(b, a, sh);
+  hi = __builtin_amdgcn_alignbit(c, b, sh);
+  return true;
 }
 
 __global__ void __launch_bounds__(kThreads)
 chunk_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nblocks,
                   int64_t* __restrict__ chunk) {
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
+  __syncthreads();
   const int64_t b0 = int64_t(blockIdx.x) * kChunk + int64_t(threadIdx.x) * kIters;
-  uint32_t tot;
-  wg_exclusive_scan(bits_of_8(rung, rt, b0, nblocks), &tot);
-  if (threadIdx.x == 0) chunk[blockIdx.x] = tot;
+  uint32_t v = bits_of_8(rung, tab, uint32_t(rt.n), b0, nblocks);
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  __shared__ uint32_t wsum[kThreads / 64];
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) tot += wsum[w];
+    chunk[blockIdx.x] = tot;
+  }
 }
 
 // One workgroup: chunk[c] (bits of chunk c) -> chunk[c] = bit offset of chunk c,
@@ -129,12 +180,33 @@ chunk_offsets_kernel(int64_t* __restrict__ chunk, int64_t nchunks, uint32_t* __r
   if (stream && threadIdx.x == 0 && (tot >> 5) < nwords) stream[tot >> 5] = 0u;
 }
 
+// Table index of every block of this thread's eight (8 bits each) and their
+// code lengths as 16-bit fields for wg_exclusive_scan8; blocks past the end
+// take the invalid entry (length 0).
+__device__ __forceinline__ void chunk_lengths(const uint8_t* __restrict__ rung, const uint4* tab,
+                                              uint32_t nr, int64_t base, int64_t nblocks,
+                                              unsigned long long& idx, ulonglong2& len) {
+  idx = 0ull;
+  len = make_ulonglong2(0ull, 0ull);
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t b = base + it * kThreads + threadIdx.x;
+    const uint32_t r = b < nblocks ? table_index(rung ? uint32_t(rung[b]) : 0u, nr) : nr;
+    idx |= (unsigned long long)r << (8 * it);
+    const unsigned long long l = (unsigned long long)tab[r].w << (16 * (it & 3));
+    if (it < 4) len.x |= l;
+    else len.y |= l;
+  }
+}
+
 __global__ void __launch_bounds__(kThreads)
 pack_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
             const int8_t* __restrict__ q, const uint8_t* __restrict__ rung, RungTable rt,
             int64_t nblocks, const int64_t* __restrict__ chunk, uint32_t* __restrict__ stream,
             int64_t nwords) {
   __shared__ uint32_t stage[kStageWords];
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
   const int64_t base = int64_t(blockIdx.x) * kChunk;
   const int64_t off0 = chunk[blockIdx.x], off1 = chunk[blockIdx.x + 1];
   const int64_t w0 = off0 >> 5;
@@ -142,22 +214,26 @@ pack_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
   const int nw = int((off1 - (w0 << 5) + 31) >> 5);
   for (int i = threadIdx.x; i < nw; i += kThreads) stage[i] = 0u;
   __syncthreads();
+  unsigned long long idx;
+  ulonglong2 len;
+  chunk_lengths(rung, tab, uint32_t(rt.n), base, nblocks, idx, len);
+  ulonglong2 tot;
+  const ulonglong2 ex = wg_exclusive_scan8(len, &tot);
   uint32_t run = shift;  // bit position inside stage
+#pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int64_t b = base + it * kThreads + threadIdx.x;
-    const int r = b < nblocks ? (rung ? int(rung[b]) : 0) : SEEDQ_MAX_RUNGS;
-    const uint32_t len = b < nblocks ? uint32_t(code_bits(rt, r)) : 0u;
-    uint32_t tot;
-    const uint32_t ex = wg_exclusive_scan(len, &tot);
-    if (len) {
-      const int K = rt.K[r], P = rt.P[r];
+    const uint4 in = tab[(idx >> (8 * it)) & 0xFFu];
+    const uint32_t pos = run + field16(ex, it);
+    run += field16(tot, it);
+    if (in.w) {
+      const int K = int(in.x), P = int(in.y);
       uint64_t code = uint64_t(seed[b] & ((1u << K) - 1u)) | (uint64_t(expo[b] & 15u) << K);
       const uint2 qw = reinterpret_cast<const uint2*>(q)[b];
       for (int j = 0; j < P; ++j) {
         const uint32_t word = j < 4 ? qw.x : qw.y;
         code |= uint64_t((word >> (8 * (j & 3))) & 15u) << (K + 4 + 4 * j);
       }
-      const uint32_t pos = run + ex;
       const int wi = int(pos >> 5), sh = int(pos & 31);
       const uint64_t lo = code << sh;
       const uint32_t hi = sh ? uint32_t(code >> (64 - sh)) : 0u;
@@ -165,7 +241,6 @@ pack_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
       if (uint32_t(lo >> 32)) atomicOr(&stage[wi + 1], uint32_t(lo >> 32));
       if (hi) atomicOr(&stage[wi + 2], hi);
     }
-    run += tot;
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nw; i += kThreads) {
@@ -178,67 +253,53 @@ pack_kernel(const uint32_t* __restrict__ seed, const uint8_t* __restrict__ expo,
   }
 }
 
-// Code of the block whose len bits start at stream bit pos (len <= 52), or
-// false when the stream ends before it.
-__device__ __forceinline__ bool read_code(const uint32_t* __restrict__ stream, int64_t nwords,
-                                          int64_t pos, int len, uint64_t& code) {
-  if (pos + len > (nwords << 5)) return false;
-  const int64_t wi = pos >> 5;
-  const int sh = int(pos & 31);
-  const uint32_t a = stream[wi];
-  const uint32_t b = wi + 1 < nwords ? stream[wi + 1] : 0u;
-  const uint32_t c = wi + 2 < nwords ? stream[wi + 2] : 0u;
-  uint64_t v = ((uint64_t(b) << 32) | a) >> sh;
-  if (sh) v |= uint64_t(c) << (64 - sh);
-  code = v & ((uint64_t(1) << len) - 1u);
-  return true;
-}
-
-// Fields of a code: seed, exponent and the mantissas as signed bytes of qw.
-__device__ __forceinline__ void split_code(uint64_t code, int K, int P, uint32_t& s, int& e,
-                                           uint2& qw) {
-  s = uint32_t(code & ((uint64_t(1) << K) - 1u));
-  e = int((code >> K) & 15u);
-  qw = make_uint2(0u, 0u);
-  for (int j = 0; j < P; ++j) {
-    const uint32_t v = uint32_t((code >> (K + 4 + 4 * j)) & 15u);
-    const uint32_t byte = (v ^ 8u) - 8u;  // sign-extend the nibble
-    if (j < 4) qw.x |= (byte & 0xFFu) << (8 * j);
-    else qw.y |= (byte & 0xFFu) << (8 * (j - 4));
-  }
-}
-
-// MODE 0: codes out (seed, exp, q); MODE 1: reconstructed weights out.
+// One-pass parse of a chunk: MODE 0 writes the codes (seed, exponent, the P
+// mantissas as bytes), MODE 1 the reconstructed weights. A block whose bits
+// are not all inside the stream, or whose rung byte is out of range, decodes
+// to seed 0 (MODE 1: NaN weights).
 template <int MODE>
 __global__ void __launch_bounds__(kThreads)
 parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t* __restrict__ rung,
              RungTable rt, int64_t nblocks, const int64_t* __restrict__ chunk,
              uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
              int8_t* __restrict__ q_out, float* __restrict__ W_hat) {
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
+  __syncthreads();
   const int64_t base = int64_t(blockIdx.x) * kChunk;
+  unsigned long long idx;
+  ulonglong2 len;
+  chunk_lengths(rung, tab, uint32_t(rt.n), base, nblocks, idx, len);
+  ulonglong2 tot;
+  const ulonglong2 ex = wg_exclusive_scan8(len, &tot);
   int64_t run = chunk[blockIdx.x];
+#pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int64_t b = base + it * kThreads + threadIdx.x;
-    const int r = b < nblocks ? (rung ? int(rung[b]) : 0) : SEEDQ_MAX_RUNGS;
-    const int len = b < nblocks ? code_bits(rt, r) : 0;
-    uint32_t tot;
-    const uint32_t ex = wg_exclusive_scan(uint32_t(len), &tot);
+    const uint4 in = tab[(idx >> (8 * it)) & 0xFFu];
+    const int64_t pos = run + field16(ex, it);
+    run += field16(tot, it);
     if (b < nblocks) {
-      const int K = len ? rt.K[r] : SEEDQ_MIN_K;
-      const int P = len ? rt.P[r] : 1;
-      uint64_t code = 0;
-      const bool ok = len && read_code(stream, nwords, run + ex, len, code);
-      uint32_t s = 0u;
-      int e = 0;
-      uint2 qw = make_uint2(0u, 0u);
-      if (ok) split_code(code, K, P, s, e, qw);
+      const int K = int(in.x), P = int(in.y);
+      uint32_t lo = 0u, hi = 0u;
+      const bool ok = read_window(stream, nwords, pos, in.w, lo, hi);
+      const uint32_t s = ok ? lo & ((1u << K) - 1u) : 0u;
+      const int e = ok ? int((lo >> K) & 15u) : 0;
+      const uint32_t qb = ok ? __builtin_amdgcn_alignbit(hi, lo, uint32_t(K + 4)) : 0u;
       if (MODE == 0) {
+        uint32_t qx = 0u, qy = 0u;
+        for (int j = 0; j < P; ++j) {
+          const uint32_t byte = uint32_t(__builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4)) & 0xFFu;
+          if (j < 4) qx |= byte << (8 * j);
+          else qy |= byte << (8 * (j - 4));
+        }
         seed_out[b] = s;
         exp_out[b] = uint8_t(e);
-        reinterpret_cast<uint2*>(q_out)[b] = qw;
+        reinterpret_cast<uint2*>(q_out)[b] = make_uint2(qx, qy);
       } else {
         int32_t acc[kC];
-        block_acc(ok ? s : 1u, K, P, qw, acc);
+        block_acc_q(ok ? s : 1u, K, P, in.z,
+                    [&](int j) { return __builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4); }, acc);
         float o[kC];
         block_weights(acc, K, e, ok && s != 0u, o);
         float4* dst = reinterpret_cast<float4*>(W_hat + b * kC);
@@ -246,10 +307,8 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
         dst[1] = make_float4(o[4], o[5], o[6], o[7]);
       }
     }
-    run += tot;
   }
 }
-
 
 // ---------------------------------------------------------------- decode-GEMV
 // y_v = W_hat x_v for nv right-hand sides, W_hat decoded from the stream on the
@@ -265,18 +324,6 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
 // d_v = sum_i fp32(acc_i) x_v[8g + i]; since w_hat_i = fp32(acc_i) 2^-(K-1+e)
 // exactly, d_v 2^-(K-1+e) is the block's partial product up to fp32 rounding.
 // A wave reduction gives y_v[r].
-
-__device__ __forceinline__ uint32_t wave_exclusive_scan(uint32_t v, uint32_t* total) {
-  const int lane = threadIdx.x & 63;
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
-  }
-  *total = __shfl(x, 63, 64);
-  return x - v;
-}
 
 __device__ __forceinline__ uint64_t wave_exclusive_scan64(uint64_t v, uint64_t* total) {
   const int lane = threadIdx.x & 63;
@@ -294,12 +341,16 @@ __device__ __forceinline__ uint64_t wave_exclusive_scan64(uint64_t v, uint64_t* 
 __global__ void __launch_bounds__(kThreads)
 row_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
                 int64_t* __restrict__ row_off) {
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
+  __syncthreads();
   const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
   if (r >= nrows) return;
   const int lane = threadIdx.x & 63;
+  const uint32_t nr = uint32_t(rt.n);
   int64_t sum = 0;
   const uint8_t* row = rung ? rung + r * G : nullptr;
-  for (int64_t g = 8 * lane; g < G; g += 8 * 64) sum += bits_of_8(row, rt, g, G);
+  for (int64_t g = 8 * lane; g < G; g += 8 * 64) sum += bits_of_8(row, tab, nr, g, G);
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) sum += __shfl_xor(sum, d, 64);
   if (lane == 0) row_off[r] = sum;
@@ -313,22 +364,12 @@ gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
                    const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
                    const int64_t* __restrict__ row_off, const float* __restrict__ x,
                    int64_t ldx, float* __restrict__ y, int64_t ldy) {
-  // (K, P, feedback mask, code length) per rung; entry rt.n (and every rung
-  // byte >= rt.n, clamped to it) is an invalid code of length 0.
-  __shared__ uint4 tab[SEEDQ_MAX_RUNGS + 1];
-  if (threadIdx.x <= SEEDQ_MAX_RUNGS) {
-    const int t = int(threadIdx.x);
-    const bool v = t < rt.n;
-    const int K = v ? rt.K[t] : SEEDQ_MIN_K;
-    const int P = v ? rt.P[t] : 1;
-    tab[t] = make_uint4(uint32_t(K), uint32_t(P), lfsr_mask(K), v ? uint32_t(K + 4 + 4 * P) : 0u);
-  }
+  __shared__ uint4 tab[kRungTable];
+  fill_rung_table(tab, rt);
   __syncthreads();
   const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
   if (r >= nrows) return;  // wave-uniform
   const int lane = threadIdx.x & 63;
-  const int64_t nbits = nwords << 5;
-  const int64_t last = nwords - 1;
   const uint32_t nr = uint32_t(rt.n);
   float acc[NV];
 #pragma unroll
@@ -341,9 +382,7 @@ gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
 #pragma unroll
     for (int k = 0; k < kGemvNB; ++k) {
       const int64_t g = g0 + 64 * k + lane;
-      const uint32_t rr = g < G ? (row ? uint32_t(row[g]) : 0u) : nr;
-      info[k] = tab[rr < nr ? rr : nr];
-      if (g >= G) info[k].w = 0u;
+      info[k] = tab[g < G ? table_index(row ? uint32_t(row[g]) : 0u, nr) : nr];
       lbits |= uint64_t(info[k].w) << (16 * k);
     }
     uint64_t tot;
@@ -356,27 +395,8 @@ gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
       if (g < G) {
         const int K = int(info[k].x), P = int(info[k].y);
         const uint32_t len = info[k].w;
-        bool ok = len != 0u && pos + int64_t(len) <= nbits;
         uint32_t lo = 0u, hi = 0u;
-        if (ok) {
-          const int64_t wi = pos >> 5;
-          const uint32_t* sp = stream + wi;
-          uint32_t a, b, c;
-          if (wi + 2 <= last) {
-            a = sp[0];
-            b = sp[1];
-            c = sp[2];
-          } else {  // the last two words of the stream
-            a = sp[0];
-            b = wi + 1 <= last ? sp[1] : 0u;
-            c = 0u;
-          }
-          // bits at and above len belong to the next block (or are zero past
-          // the stream's end); no field below reads them
-          const uint32_t sh = uint32_t(pos) & 31u;
-          lo = __builtin_amdgcn_alignbit(b, a, sh);
-          hi = __builtin_amdgcn_alignbit(c, b, sh);
-        }
+        bool ok = read_window(stream, nwords, pos, len, lo, hi);
         const uint32_t s = lo & ((1u << K) - 1u);
         const int e = int((lo >> K) & 15u);
         const uint32_t qb = __builtin_amdgcn_alignbit(hi, lo, uint32_t(K + 4));
