@@ -273,20 +273,24 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
   ulonglong2 tot;
   const ulonglong2 ex = wg_exclusive_scan8(len, &tot);
   int64_t run = chunk[blockIdx.x];
+  // MODE 1: an iteration's 256 blocks are 8 KB of contiguous weights, staged
+  // in LDS (two buffers, so one barrier per iteration) and stored so that
+  // every store instruction of a wave writes 1 KB without gaps.
+  __shared__ float4 stage[MODE == 1 ? 2 : 1][2 * kThreads];
 #pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int64_t b = base + it * kThreads + threadIdx.x;
     const uint4 in = tab[(idx >> (8 * it)) & 0xFFu];
     const int64_t pos = run + field16(ex, it);
     run += field16(tot, it);
-    if (b < nblocks) {
+    if (MODE == 1 || b < nblocks) {  // MODE 1: every thread, for the barrier
       const int K = int(in.x), P = int(in.y);
       uint32_t lo = 0u, hi = 0u;
       const bool ok = read_window(stream, nwords, pos, in.w, lo, hi);
       const uint32_t s = ok ? lo & ((1u << K) - 1u) : 0u;
       const int e = ok ? int((lo >> K) & 15u) : 0;
       const uint32_t qb = ok ? __builtin_amdgcn_alignbit(hi, lo, uint32_t(K + 4)) : 0u;
-      if (MODE == 0) {
+      if constexpr (MODE == 0) {
         uint32_t qx = 0u, qy = 0u;
         for (int j = 0; j < P; ++j) {
           const uint32_t byte = uint32_t(__builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4)) & 0xFFu;
@@ -302,9 +306,14 @@ parse_kernel(const uint32_t* __restrict__ stream, int64_t nwords, const uint8_t*
                     [&](int j) { return __builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4); }, acc);
         float o[kC];
         block_weights(acc, K, e, ok && s != 0u, o);
-        float4* dst = reinterpret_cast<float4*>(W_hat + b * kC);
-        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-        dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+        float4* buf = stage[it & 1];
+        buf[2 * threadIdx.x] = make_float4(o[0], o[1], o[2], o[3]);
+        buf[2 * threadIdx.x + 1] = make_float4(o[4], o[5], o[6], o[7]);
+        __syncthreads();
+        const int64_t b0 = base + it * kThreads;
+        const int64_t nlive = nblocks - b0 < kThreads ? nblocks - b0 : kThreads;
+        float4* dst = reinterpret_cast<float4*>(W_hat + b0 * kC);
+        for (int i = threadIdx.x; i < 2 * nlive; i += kThreads) dst[i] = buf[i];
       }
     }
   }

@@ -178,3 +178,34 @@ def test_stream_argument_errors_need_no_gpu(sq):
                                      ws, None) == -2
     # W_hat misaligned
     assert L.seedq_decompress_stream(256, 64, None, 1, R, 8, 64, 8, 264, 256, ws, None) == -1
+
+
+@pytest.mark.parametrize("nrows,ncols", [(0, 64), (8, 0), (-1, 64), (8, -8)])
+def test_empty_and_negative_shapes_are_argument_errors(sq, nrows, ncols):
+    # every matrix entry point rejects an empty or negative shape before it
+    # touches a pointer (the dummy addresses below are never dereferenced)
+    L = sq.lib()
+    b = (sq.BasesRef * 1)(sq.BasesRef(16, 3, 256))
+    R = sq._rungs(((16, 3),))
+    ws = 1 << 20
+    assert L.seedq_compress(256, nrows, ncols, 8, None, 1, b, 256, 256, 256, None, None, 0,
+                            None) == -1
+    assert L.seedq_decompress(256, 256, 256, None, 1, R, nrows, ncols, 8, 256, None, None) == -1
+    assert L.seedq_pack(256, 256, 256, None, 1, R, nrows, ncols, 8, 256, 256, 256, ws, None) == -1
+    assert L.seedq_unpack(256, 256, None, 1, R, nrows, ncols, 8, 256, 256, 256, 256, ws,
+                          None) == -1
+    assert L.seedq_decompress_stream(256, 256, None, 1, R, nrows, ncols, 8, 256, 256, ws,
+                                     None) == -1
+    assert L.seedq_gemv_stream(256, 256, None, 1, R, nrows, ncols, 8, 1, 256, 256, 256, ws,
+                               None) == -1
+    assert L.seedq_sq_gemv(256, nrows, ncols, 256, 0, 256, 256, ws, None) == -1
+    assert L.seedq_column_stats(256, nrows, ncols, 256, 256, None) == -1
+    assert L.seedq_permute_columns(256, nrows, ncols, 256, 0, 512, None) == -1
+    assert L.seedq_extract_columns(256, nrows, ncols, 1, 256, 256, None) == -1
+    assert L.seedq_apply_columns(256, nrows, ncols, 1, 256, 256, None) == -1
+    assert sq.seedq_stream_workspace_bytes(nrows, ncols) == 0
+    assert sq.seedq_sq_gemv_workspace_bytes(nrows, ncols, 0) == 0
+    with pytest.raises(sq.SeedqError) as e:
+        sq.plan_schedule(max(nrows, 0), max(ncols, 0), ((16, 3),), None, 4.0,
+                         np.ones(max(ncols, 0), dtype=np.float32))
+    assert e.value.code in (-1, -3)

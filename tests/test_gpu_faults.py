@@ -53,3 +53,18 @@ def test_fault_study_payload_faults_stay_in_their_block():
     assert len(payload) == 4 and all(0 < r["N_flip"] <= 8 for r in payload)
     assert table and all(r["table_checksum_detects"] for r in table)
     assert any(r.get("N_flip", 0) > 1000 for r in table)
+
+
+def test_footprint_of_nothing_is_zero():
+    # n = 0: the kernels still run once and write a zero count and zero sums
+    # over whatever the outputs held before
+    import torch
+    import paper_2609_38477_amd as sq
+    a = torch.zeros(64, dtype=torch.float32, device="cuda")
+    cnt = torch.full((1,), 7, dtype=torch.int64, device="cuda")
+    sums = torch.full((2,), 3.0, dtype=torch.float64, device="cuda")
+    nws = sq.seedq_footprint_workspace_bytes()
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    sq.seedq_footprint(a, a, 0, cnt, sums, ws, nws, None)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == 0 and sums.cpu().tolist() == [0.0, 0.0]

@@ -97,6 +97,19 @@ def test_fp16_escape_columns(sq):
     assert np.count_nonzero(np.delete(z, cols, 1)) == 0
 
 
+def test_zero_columns_and_zero_variances_are_no_ops(sq):
+    import torch
+    W = torch.arange(24, dtype=torch.float32, device="cuda").reshape(3, 8)
+    before = W.clone()
+    sq.seedq_extract_columns(W, 3, 8, 0, None, None)
+    sq.seedq_apply_columns(W, 3, 8, 0, None, None)
+    v = torch.ones(4, dtype=torch.float64, device="cuda")
+    out = torch.full((4,), 5.0, dtype=torch.float64, device="cuda")
+    sq.seedq_expect_silu_sq(v, 0, 128, out)
+    torch.cuda.synchronize()
+    assert torch.equal(W, before) and out.cpu().tolist() == [5.0] * 4
+
+
 def test_layer_importance_matches_oracle(sq):
     from paper_2609_38477_amd import frontend
     L = synthetic.synthetic_layer()
