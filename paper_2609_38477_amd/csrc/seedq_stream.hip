@@ -143,18 +143,29 @@ chunk_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nblock
 
 // One workgroup: chunk[c] (bits of chunk c) -> chunk[c] = bit offset of chunk c,
 // chunk[nchunks] = total bits, in place. With a stream, also clears the words
-// that hold a chunk boundary, the only words two chunks both write.
-__global__ void __launch_bounds__(kThreads)
+// that hold a chunk boundary, the only words two chunks both write. Each of the
+// 1024 threads owns a contiguous run of chunks and reads it 8 values at a time
+// with independent loads, so the pass is not one load latency per chunk.
+constexpr int kScanThreads = 1024;
+constexpr int kScanBatch = 8;
+
+__global__ void __launch_bounds__(kScanThreads)
 chunk_offsets_kernel(int64_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ stream,
                      int64_t nwords) {
-  __shared__ int64_t part[kThreads / 64];
-  const int64_t per = (nchunks + kThreads - 1) / kThreads;
+  __shared__ int64_t part[kScanThreads / 64];
+  const int64_t per = (nchunks + kScanThreads - 1) / kScanThreads;
   const int64_t c0 = min(nchunks, int64_t(threadIdx.x) * per);
   const int64_t c1 = min(nchunks, c0 + per);
   int64_t s = 0;
-  for (int64_t c = c0; c < c1; ++c) s += chunk[c];
+  for (int64_t c = c0; c < c1; c += kScanBatch) {
+    int64_t v[kScanBatch];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) v[k] = c + k < c1 ? chunk[c + k] : 0;
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) s += v[k];
+  }
   // exclusive scan of the per-thread sums: within each wave by shuffles, then
-  // across the four waves
+  // across the waves
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int64_t x = s;
 #pragma unroll
@@ -166,16 +177,23 @@ chunk_offsets_kernel(int64_t* __restrict__ chunk, int64_t nchunks, uint32_t* __r
   __syncthreads();
   int64_t run = x - s, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kThreads / 64; ++w) {
+  for (int w = 0; w < kScanThreads / 64; ++w) {
     run += w < wave ? part[w] : 0;
     tot += part[w];
   }
   if (threadIdx.x == 0) chunk[nchunks] = tot;
-  for (int64_t c = c0; c < c1; ++c) {
-    const int64_t v = chunk[c];
-    chunk[c] = run;
-    if (stream && (run >> 5) < nwords) stream[run >> 5] = 0u;
-    run += v;
+  for (int64_t c = c0; c < c1; c += kScanBatch) {
+    int64_t v[kScanBatch];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) v[k] = c + k < c1 ? chunk[c + k] : 0;
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      if (c + k < c1) {
+        chunk[c + k] = run;
+        if (stream && (run >> 5) < nwords) stream[run >> 5] = 0u;
+        run += v[k];
+      }
+    }
   }
   if (stream && threadIdx.x == 0 && (tot >> 5) < nwords) stream[tot >> 5] = 0u;
 }
@@ -459,7 +477,7 @@ static hipError_t launch_offsets(const uint8_t* d_rung, const RungTable& rt, int
   if (nchunks > 0)
     hipLaunchKernelGGL(chunk_bits_kernel, dim3(unsigned(nchunks)), dim3(kThreads), 0, stream, d_rung,
                        rt, nblocks, chunk);
-  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kThreads), 0, stream, chunk, nchunks,
+  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kScanThreads), 0, stream, chunk, nchunks,
                      zero_stream, nwords);
   return hipGetLastError();
 }
@@ -503,7 +521,7 @@ hipError_t launch_gemv_stream(const uint32_t* d_stream, int64_t nwords, const ui
   const unsigned grid = unsigned((nrows + kThreads / 64 - 1) / (kThreads / 64));
   hipLaunchKernelGGL(row_bits_kernel, dim3(grid), dim3(kThreads), 0, stream, d_rung, rt, nrows, G,
                      row_off);
-  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kThreads), 0, stream, row_off, nrows,
+  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(kScanThreads), 0, stream, row_off, nrows,
                      nullptr, int64_t(0));
   switch (nv) {
     case 1:
