@@ -50,6 +50,16 @@ constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
 constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
+// With the residual filter up to 63 filtered and 63 new entries wait before a
+// pair of block tiles adds its at most 2 x 1024.
+constexpr int kQCapFiltered = 128 + 2 * 1024;
+// Rungs that use the residual filter: it defers exact evaluations until 64
+// filtered entries wait, which pays only where most survivors of the matrix
+// core's screen fail the fp32 residual (measured on 2.1 M blocks: (16,6) and
+// (15,6) faster, (14,6) and below slower, P <= 5 no gain).
+constexpr int kFilterMinP = 6;
+constexpr int kFilterMinK = 15;
+constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane masks
 constexpr int kPilotTiles = 1;
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
@@ -454,13 +464,13 @@ template <int P>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
 search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
-                   const double* __restrict__ pinv64, const half8* __restrict__ pi16,
-                   int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
-                   uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                   float* __restrict__ err_out) {
+                   const double* __restrict__ pinv64, const float* __restrict__ q32,
+                   const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
+                   uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
+                   int8_t* __restrict__ q_out, float* __restrict__ err_out) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
-  __shared__ uint32_t queue_all[kWaves][kQCap];
+  __shared__ uint32_t queue_all[kWaves][kQCapFiltered];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -527,14 +537,79 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     }
   };
 
-  int qcount = 0;  // wave-uniform
-  // Evaluate the top min(64, qcount) entries, one per lane, until fewer than
-  // min_batch remain; then rebuild the block data and thresholds.
-  auto flush = [&](int min_batch) __attribute__((always_inline)) {
+  // The queue holds nf entries that passed the residual filter below (at the
+  // bottom) and qcount - nf new ones above them (wave-uniform counts).
+  int qcount = 0, nf = 0;
+  // Residual filter of the new entries: the least-squares residual is
+  // recomputed in fp32 from the orthonormal basis, ||w||^2 - ||Q_s^T w||^2,
+  // with a margin of 2^-16 ||w||^2 for its rounding instead of the matrix
+  // core's gamma (the bound the vector engine screens with). An entry that can
+  // still reach its block's best error moves down to the filtered region; the
+  // others are dropped, as are no-op entries (seed 0).
+  auto filter = [&]() __attribute__((always_inline)) {
+    if (P < kFilterMinP || K < kFilterMinK) {
+      nf = qcount;  // every entry goes to the exact evaluation (no-op entries skip it)
+      return;
+    }
     __threadfence_block();
-    while (qcount >= min_batch && qcount > 0) {
-      const int e = qcount < 64 ? qcount : 64;
-      const int base = qcount - e;
+    for (int i = nf; i < qcount; i += 64) {
+      const int e = qcount - i < 64 ? qcount - i : 64;
+      uint32_t ent = 0u;
+      bool keep = false;
+      if (lane < e) {
+        ent = queue[i + lane];
+        const uint32_t seed = ent >> 8;
+        const int slot = int(ent & 0x7Fu);
+        const unsigned long long key = keys[slot];
+        keep = seed != 0u;
+        if (keep && !(ent & kFinal) && key != ~0ull) {
+          float w[kC];
+          load_block(W, blk[slot], true, w);
+          float amax = 0.f;
+#pragma unroll
+          for (int k = 0; k < kC; ++k) amax = fmaxf(amax, fabsf(w[k]));
+          const int ex = ilogbf(amax);  // queued blocks are not all zero
+          float ws[kC], ww = 0.f;
+#pragma unroll
+          for (int k = 0; k < kC; ++k) {
+            ws[k] = ldexpf(w[k], -ex);
+            ww = fmaf(ws[k], ws[k], ww);
+          }
+          const float4* Qs = reinterpret_cast<const float4*>(q32 + int64_t(seed - 1) * (P * kC));
+          float ss = 0.f;
+#pragma unroll
+          for (int p = 0; p < P; ++p) {
+            const float4 a = Qs[2 * p], b = Qs[2 * p + 1];
+            float c = a.x * ws[0];
+            c = fmaf(a.y, ws[1], c);
+            c = fmaf(a.z, ws[2], c);
+            c = fmaf(a.w, ws[3], c);
+            c = fmaf(b.x, ws[4], c);
+            c = fmaf(b.y, ws[5], c);
+            c = fmaf(b.z, ws[6], c);
+            c = fmaf(b.w, ws[7], c);
+            ss = fmaf(c, c, ss);
+          }
+          const double bound = key_error(key) * (1.0 + 0x1p-27);
+          const float bu = __double2float_ru(ldexp(bound, -2 * ex)) * (1.0f + 0x1p-20f);
+          keep = ss >= ww * (1.0f - 0x1p-16f) - bu;
+        }
+      }
+      const uint64_t mk = ballot(keep);
+      if (keep) queue[nf + lanes_below(mk)] = ent;
+      nf += __popcll(mk);
+    }
+    qcount = nf;
+    __threadfence_block();
+  };
+  // Evaluate the top min(64, nf) filtered entries, one per lane, until fewer
+  // than min_batch remain; after any evaluation rebuild the block data and
+  // thresholds. Returns whether it evaluated (wave-uniform).
+  auto exact = [&](int min_batch) __attribute__((always_inline)) {
+    bool ran = false;
+    while (nf >= min_batch && nf > 0) {
+      const int e = nf < 64 ? nf : 64;
+      const int base = nf - e;
       if (lane < e) {
         const uint32_t ent = queue[base + lane];
         const uint32_t seed = ent >> 8;
@@ -563,10 +638,19 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
           }
         }
       }
-      qcount = base;
+      nf = base;
+      ran = true;
     }
-    __threadfence_block();
-    setup();
+    qcount = nf;
+    if (ran) {
+      __threadfence_block();
+      setup();
+    }
+    return ran;
+  };
+  auto flush = [&](int min_batch) __attribute__((always_inline)) {
+    filter();
+    exact(min_batch);
   };
 
   const half8* A = pi16;
@@ -600,22 +684,43 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // Queue the candidates of block tile nt whose bound passes. At most 1024 per
   // block tile; fewer than 64 are queued before a pair of block tiles, so the
   // 2 x 1024 of one pair always fit.
+  // At P >= 5 a few percent of the candidates pass, so most of the 16 seeds of
+  // a tile have a passing lane: there each lane builds its mask of passing
+  // seeds and queues one set bit per round (at P = 6 only for K >= 15, where
+  // it measured faster). Otherwise one ballot per seed.
+  const bool mask_check = P >= kMaskCheckMinP && (P < kFilterMinP || K >= kFilterMinK);
   auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
                    __attribute__((always_inline)) {
     constexpr int nt = decltype(ntc)::value;
-    if (ballot(any) != 0ull) {
+    if (ballot(any) == 0ull) return;
+    if (P >= kMaskCheckMinP && mask_check) {
+      uint32_t m = 0u;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const bool pass = acc[j] >= thr[nt];
-        const uint64_t mk = ballot(pass);
-        if (mk != 0ull) {
-          if (pass) {
-            const uint32_t seed = seed_of(seedbase, j, h);
-            queue[qcount + lanes_below(mk)] =
-                ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
-          }
-          qcount += __popcll(mk);
+      for (int j = 0; j < 16; ++j) m |= (acc[j] >= thr[nt] ? 1u : 0u) << j;
+      for (;;) {
+        const uint64_t mk = ballot(m != 0u);
+        if (mk == 0ull) break;
+        if (m != 0u) {
+          const uint32_t seed = seed_of(seedbase, __builtin_ctz(m), h);
+          queue[qcount + lanes_below(mk)] =
+              ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
+          m &= m - 1u;
         }
+        qcount += __popcll(mk);
+      }
+      return;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const bool pass = acc[j] >= thr[nt];
+      const uint64_t mk = ballot(pass);
+      if (mk != 0ull) {
+        if (pass) {
+          const uint32_t seed = seed_of(seedbase, j, h);
+          queue[qcount + lanes_below(mk)] =
+              ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
+        }
+        qcount += __popcll(mk);
       }
     }
   };
@@ -650,10 +755,12 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       if ((ballot(p0) | ballot(p1)) != 0ull) {
         check(I0{}, acc0, p0, seedbase);
         check(I1{}, acc1, p1, seedbase);
-        if (qcount >= 64) {
-          flush(64);
-          load_tile(T, c);
-          load_tile(To, o);
+        if (qcount - nf >= 64) {
+          filter();
+          if (exact(64)) {
+            load_tile(T, c);
+            load_tile(To, o);
+          }
         }
       }
     }
@@ -665,9 +772,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       if ((ballot(p2) | ballot(p3)) != 0ull) {
         check(I2{}, acc2, p2, seedbase);
         check(I3{}, acc3, p3, seedbase);
-        if (qcount >= 64) {
-          flush(64);
-          load_tile(To, o);
+        if (qcount - nf >= 64) {
+          filter();
+          if (exact(64)) load_tile(To, o);
         }
       }
     }
@@ -737,8 +844,9 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.err_out = d_err;
   if constexpr (P >= 4)
     hipLaunchKernelGGL(search_mfma_remat_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0,
-                       stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
-                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
+                       stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
+                       reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
+                       a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
   else
     hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
                        a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,

@@ -210,6 +210,20 @@ def test_search_k20_sampled(sq, oq, torch):
                  q.cpu().numpy(), err.cpu().numpy(), "K20")
 
 
+@pytest.mark.parametrize("K,P,nb", [(16, 6, 48), (15, 6, 64), (16, 5, 48)])
+def test_search_dense_survivor_rungs(sq, oq, torch, K, P, nb):
+    # rungs where a few percent of all seeds pass the matrix core's screen: the
+    # lane-mask enqueue (P >= 5) and, at P = 6 and K >= 15, the fp32 residual
+    # filter in front of the exact evaluation; 48 or 64 blocks leave part of a
+    # wave's four 32-block tiles empty; heavy-tailed blocks among them
+    W = synthetic.weights(1, 8 * nb, 0.02, key=60 + K + P, outlier_frac=0.05)
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(_dev(torch, W), [b])
+    torch.cuda.synchronize()
+    check_search(oq, W, K, P, seed.cpu().numpy().view(np.uint32), e.cpu().numpy(),
+                 q.cpu().numpy(), err.cpu().numpy(), f"K{K}P{P}")
+
+
 def test_search_full_size_attention_sampled(sq, oq, torch):
     # 4096 x 4096 at (16, 3), in the launch configuration the benchmark times;
     # the oracle checks an evenly spaced sample of 192 blocks
