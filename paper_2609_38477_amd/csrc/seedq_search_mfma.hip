@@ -16,7 +16,9 @@
 //
 // Survivors. Each wave queues its passing (seed, block) pairs in LDS and
 // evaluates them 64 at a time, one per lane, with the exact fp64 evaluation
-// shared with the other engine. Per-block bests live in LDS as 64-bit keys
+// shared with the other engine. At P <= 3 a lane whose fold passes first
+// stores its 16 bounds as a record; records are turned into queued seeds 64
+// at a time against the thresholds of that moment. Per-block bests live in LDS as 64-bit keys
 // (error bits, seed in the low 24 bits) updated with atomic minimum, so the
 // result does not depend on the order in which survivors are evaluated; ties
 // within 2^-28 relative go to the smaller seed. A pilot pass over the first
@@ -189,8 +191,19 @@ SEEDQ_INLINE int lanes_below(uint64_t mask) {
 constexpr uint32_t kFinal = 0x80u;
 static_assert(kSlots <= 128, "slot must fit 7 bits");
 
+// Walk survivors of the P <= 3 kernel are first kept as records: a lane whose
+// fold passes stores its 16 bounds with the seed tile, its half and the block
+// slot (one 64-byte row and one meta word in LDS; meta = tile << 8 | half << 7
+// | slot). Records become candidates 64 at a time, each compared with its
+// block's threshold of that moment, so the per-seed ballots run once per 64
+// records instead of once per passing block tile, and records whose block has
+// meanwhile found a better code drop out before the exact evaluation.
+constexpr int kRecFlush = 32;                 // records waiting after a pair of block tiles
+constexpr int kRecCap = kRecFlush + 64;       // one block tile adds at most 64
+constexpr int kQCapRec = 64 + 64 * 16;        // < 64 waiting + one round of 64 records
+
 template <int P>
-__global__ void __launch_bounds__(kWaves * 64)
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3)))
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
@@ -199,14 +212,23 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    float* __restrict__ err_out) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
-  __shared__ uint32_t queue_all[kWaves][kQCap];
+  __shared__ float thr_base_all[kWaves][kSlots];   // ||w||^2 (1 - gamma) in accumulator units
+  __shared__ int8_t ex_all[kWaves][kSlots];        // power-of-two scaling of the block
+  __shared__ float4 rec_all[kWaves][kRecCap][4];   // 16 bounds per record
+  __shared__ uint32_t meta_all[kWaves][kRecCap];
+  __shared__ uint32_t queue_all[kWaves][kQCapRec];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // wave-uniform, so that the per-wave LDS addresses are scalar
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int n = lane & 31;   // block column of the MFMA tile
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
   unsigned long long* keys = keys_all[wave];
   int32_t* blk = blk_all[wave];
+  float* slot_thr = thr_base_all[wave];
+  int8_t* slot_ex = ex_all[wave];
+  float4 (*rec)[4] = rec_all[wave];
+  uint32_t* meta = meta_all[wave];
   uint32_t* queue = queue_all[wave];
 
   int64_t begin = 0, count = nblocks;
@@ -220,8 +242,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 
   // ---------------------------------------------------------------- prologue
   half8 bop[kNB][3];
-  float thr[kNB], thr_base[kNB];
-  int ex[kNB];
+  float thr[kNB];
   bool active[kNB], valid[kNB];
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
@@ -234,15 +255,13 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 #pragma unroll
     for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
     active[nt] = valid[nt] && amax > 0.f;
-    ex[nt] = active[nt] ? ilogbf(amax) : 0;
+    const int ex = active[nt] ? ilogbf(amax) : 0;
     float ws[kC], ww = 0.f;
 #pragma unroll
     for (int i = 0; i < kC; ++i) {
-      ws[i] = ldexpf(w[i], -ex[nt]);
+      ws[i] = ldexpf(w[i], -ex);
       ww = fmaf(ws[i], ws[i], ww);
     }
-    // thresholds live in accumulator units (both operands carry 2^12)
-    thr_base[nt] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
     thr[nt] = active[nt] ? -INFINITY : INFINITY;
     bop[nt][0] = b_fragment<0>(ws, h);
     bop[nt][1] = b_fragment<1>(ws, h);
@@ -250,14 +269,32 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     if (h == 0) {
       keys[nt * 32 + n] = ~0ull;
       blk[nt * 32 + n] = int32_t(b);
+      // thresholds live in accumulator units (both operands carry 2^12)
+      slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+      slot_ex[nt * 32 + n] = int8_t(ex);
     }
   }
   __threadfence_block();
 
+  // Screening threshold of slot s from its key: a bound passes when it can
+  // reach the block's best exact error so far (-inf before the first one).
+  auto slot_threshold = [&](int s) __attribute__((always_inline)) {
+    const unsigned long long key = keys[s];
+    if (key == ~0ull) return -INFINITY;
+    const double bound = key_error(key) * (1.0 + 0x1p-27);
+    return slot_thr[s] - __double2float_ru(ldexp(bound, 24 - 2 * int(slot_ex[s])));
+  };
+  auto refresh = [&]() __attribute__((always_inline)) {
+    __threadfence_block();
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt)
+      if (active[nt]) thr[nt] = slot_threshold(nt * 32 + n);
+  };
+
   int qcount = 0;  // wave-uniform
-  // Evaluate the top min(64, qcount) entries, one per lane, until fewer than
-  // min_batch remain; then rebuild the screening thresholds from the keys.
-  auto flush = [&](int min_batch) __attribute__((always_inline)) {
+  // Evaluate the top min(64, qcount) candidates, one per lane, until fewer
+  // than min_batch remain.
+  auto evaluate = [&](int min_batch) __attribute__((always_inline)) {
     __threadfence_block();
     while (qcount >= min_batch && qcount > 0) {
       const int e = qcount < 64 ? qcount : 64;
@@ -293,115 +330,116 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       qcount = base;
     }
     __threadfence_block();
-#pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const unsigned long long key = keys[nt * 32 + n];
-      if (active[nt] && key != ~0ull) {
-        const double bound = key_error(key) * (1.0 + 0x1p-27);
-        thr[nt] = thr_base[nt] - __double2float_ru(ldexp(bound, 24 - 2 * ex[nt]));
+  };
+
+  int nrec = 0;  // wave-uniform
+  // Records -> candidates: lane l takes record base + l of the top 64 and
+  // compares its 16 bounds with the block's current threshold; one ballot per
+  // seed row queues the passing seeds. Full batches are evaluated after each
+  // round of records; the walk's thresholds are refreshed at the end.
+  auto process = [&]() __attribute__((always_inline)) {
+    __threadfence_block();
+    while (nrec > 0) {
+      const int e = nrec < 64 ? nrec : 64;
+      const int base = nrec - e;
+      const bool live = lane < e;
+      uint32_t m = 0u;
+      float t = INFINITY;
+      float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0, r2 = r0, r3 = r0;
+      if (live) {
+        m = meta[base + lane];
+        t = slot_threshold(int(m & 0x7Fu));
+        r0 = rec[base + lane][0];
+        r1 = rec[base + lane][1];
+        r2 = rec[base + lane][2];
+        r3 = rec[base + lane][3];
       }
+      const float bnd[16] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w,
+                             r2.x, r2.y, r2.z, r2.w, r3.x, r3.y, r3.z, r3.w};
+      const uint32_t seedbase = (m >> 8) * 32u + 1u;
+      const int hh = int((m >> 7) & 1u);
+      const uint32_t slot = m & 0x7Fu;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool pass = bnd[j] >= t;   // t = +inf on lanes without a record
+        const uint64_t mk = ballot(pass);
+        if (mk != 0ull) {
+          if (pass) {
+            const uint32_t seed = seed_of(seedbase, j, hh);
+            queue[qcount + lanes_below(mk)] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
+          }
+          qcount += __popcll(mk);
+        }
+      }
+      nrec = base;
+      if (qcount >= 64) evaluate(64);
     }
+    refresh();
   };
 
   const half8* A = pi16;
 
   // ---------------------------------------------------------------- pilot
-  // Over the first tile(s) each lane tracks its seed of smallest bound; their
+  // Over the first tile each lane tracks its seed of smallest bound; their
   // exact errors start every block's best. (Longer pilots cost more matrix
   // time than the survivors they save.)
   {
-    const int64_t npilot = ntiles < kPilotTiles ? ntiles : kPilotTiles;
-    float pm[kNB];
-    uint32_t ps[kNB];
+    const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
-      pm[nt] = -INFINITY;
-      ps[nt] = 0u;
-    }
-    for (int64_t T = 0; T < npilot; ++T) {
-      const half8 a0 = A[T * 192 + lane], a1 = A[T * 192 + 64 + lane], a2 = A[T * 192 + 128 + lane];
-      const uint32_t seedbase = uint32_t(T) * 32u + 1u;
+      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+      const float mx = fold_max(acc);
+      int jb = 15;
 #pragma unroll
-      for (int nt = 0; nt < kNB; ++nt) {
-        const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
-        const float m = fold_max(acc);
-        if (m > pm[nt]) {
-          int jb = 15;
-#pragma unroll
-          for (int j = 14; j >= 0; --j)
-            if (acc[j] == m) jb = j;
-          const uint32_t sd = seed_of(seedbase, jb, h);
-          if (sd <= nseeds) {
-            pm[nt] = m;
-            ps[nt] = sd;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const bool put = active[nt] && ps[nt] != 0u;
+      for (int j = 14; j >= 0; --j)
+        if (acc[j] == mx) jb = j;
+      // seeds 1..32 all exist (K >= 8)
+      const uint32_t sd = seed_of(1u, jb, h);
+      const bool put = active[nt];
       const uint64_t mk = ballot(put);
-      if (put) queue[qcount + lanes_below(mk)] = (ps[nt] << 8) | uint32_t(nt * 32 + n);
+      if (put) queue[qcount + lanes_below(mk)] = (sd << 8) | uint32_t(nt * 32 + n);
       qcount += __popcll(mk);
+      if (qcount >= 64) evaluate(64);
     }
-    flush(1);
+    evaluate(1);
+    refresh();
   }
 
   // ---------------------------------------------------------------- seed walk
-  // Queue the candidates of block tile nt whose bound passes. At most 1024 per
-  // block tile; fewer than 64 are queued before a pair of block tiles, so the
-  // 2 x 1024 of one pair always fit.
-  auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
-                   __attribute__((always_inline)) {
-    constexpr int nt = decltype(ntc)::value;
-    if (ballot(any) != 0ull) {
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const bool pass = acc[j] >= thr[nt];
-        const uint64_t mk = ballot(pass);
-        if (mk != 0ull) {
-          if (pass) {
-            const uint32_t seed = seed_of(seedbase, j, h);
-            queue[qcount + lanes_below(mk)] =
-                ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
-          }
-          qcount += __popcll(mk);
-        }
-      }
+  // Lanes of block tile nt whose fold passed store their 16 bounds as records.
+  auto record = [&](int nt, const floatx16& acc, bool pass, uint32_t T)
+                    __attribute__((always_inline)) {
+    const uint64_t mk = ballot(pass);
+    if (mk == 0ull) return;
+    if (pass) {
+      const int r = nrec + lanes_below(mk);
+      rec[r][0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      rec[r][1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      rec[r][2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+      rec[r][3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      meta[r] = (T << 8) | (uint32_t(h) << 7) | uint32_t(nt * 32 + n);
     }
+    nrec += __popcll(mk);
   };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
   static_assert(kNB == 4, "the walk below unrolls four block tiles");
 
   // One seed tile against the four block tiles: two block tiles at a time,
   // six products to the matrix core, then the folds, one branch per pair.
+  // Before each block tile's records at most kRecCap - 64 are waiting.
   auto tile = [&](const half8& a0, const half8& a1, const half8& a2, int64_t T)
                   __attribute__((always_inline)) {
-    const uint32_t seedbase = uint32_t(T) * 32u + 1u;
-    {
-      const floatx16 acc0 = bounds(a0, a1, a2, bop[0]);
-      const floatx16 acc1 = bounds(a0, a1, a2, bop[1]);
-      const bool p0 = fold_max(acc0) >= thr[0];
-      const bool p1 = fold_max(acc1) >= thr[1];
+    const uint32_t t32 = uint32_t(T);
+#pragma unroll
+    for (int pr = 0; pr < 2; ++pr) {
+      const floatx16 acc0 = bounds(a0, a1, a2, bop[2 * pr]);
+      const floatx16 acc1 = bounds(a0, a1, a2, bop[2 * pr + 1]);
+      const bool p0 = fold_max(acc0) >= thr[2 * pr];
+      const bool p1 = fold_max(acc1) >= thr[2 * pr + 1];
       if ((ballot(p0) | ballot(p1)) != 0ull) {
-        check(I0{}, acc0, p0, seedbase);
-        check(I1{}, acc1, p1, seedbase);
-        if (qcount >= 64) flush(64);
-      }
-    }
-    {
-      const floatx16 acc2 = bounds(a0, a1, a2, bop[2]);
-      const floatx16 acc3 = bounds(a0, a1, a2, bop[3]);
-      const bool p2 = fold_max(acc2) >= thr[2];
-      const bool p3 = fold_max(acc3) >= thr[3];
-      if ((ballot(p2) | ballot(p3)) != 0ull) {
-        check(I2{}, acc2, p2, seedbase);
-        check(I3{}, acc3, p3, seedbase);
-        if (qcount >= 64) flush(64);
+        record(2 * pr, acc0, p0, t32);
+        if (nrec > kRecCap - 64) process();
+        record(2 * pr + 1, acc1, p1, t32);
+        if (nrec >= kRecFlush) process();
       }
     }
   };
@@ -428,7 +466,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     }
     if (T + 1 < ntiles) tile(y0, y1, y2, T + 1);
   }
-  flush(1);
+  process();
+  evaluate(1);
 
   // ---------------------------------------------------------------- results
   // the winning seed of every block, evaluated once more to emit its code
@@ -452,7 +491,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       if (err_out) err_out[b] = 0.f;
     }
   }
-  flush(1);
+  evaluate(1);
 }
 
 // The same search for P >= 4, where the fp64 evaluation needs more registers:

@@ -300,11 +300,13 @@ def test_seed_bit_flip_footprint(sq, torch):
     assert diff.sum() <= 8
 
 
-def test_search_full_size_three_rungs_sampled(sq, oq, torch):
-    # 4096 x 11008 at 3.5 bits per weight over (12,2)/(16,3)/(20,4), with the
-    # schedule, compaction and one search launch per rung exactly as the
-    # benchmark runs them; the oracle checks evenly spaced blocks of every rung
-    wl = synthetic.WORKLOADS["reduced"]
+@pytest.mark.parametrize("name", ["reduced", "mlp_up", "l70b"])
+def test_search_full_size_three_rungs_sampled(sq, oq, torch, name):
+    # 4096 x 11008 at 3.5 bits per weight, 4096 x 14336 and 8192 x 28672 at 4.0,
+    # over (12,2)/(16,3)/(20,4), with the schedule, compaction and one search
+    # launch per rung exactly as the benchmark runs them; the oracle checks
+    # evenly spaced blocks of every rung
+    wl = synthetic.WORKLOADS[name]
     W = synthetic.workload_weights(wl)
     a = synthetic.importance_profile(wl.ncols)
     rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
@@ -325,4 +327,4 @@ def test_search_full_size_three_rungs_sampled(sq, oq, torch):
         n = 12 if K == 20 else 48
         idx = sel[np.linspace(0, len(sel) - 1, n).astype(np.int64)]
         check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx],
-                     f"reduced rung{r}")
+                     f"{name} rung{r}")
