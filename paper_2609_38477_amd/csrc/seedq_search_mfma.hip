@@ -63,6 +63,17 @@ constexpr int kFilterMinP = 6;
 constexpr int kFilterMinK = 15;
 constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane masks
 constexpr int kPilotTiles = 1;
+// P = 4 in the rebuilding kernel keeps walk survivors as records (16 bounds
+// and a meta word each) in its per-wave pool: 16 records waiting after a pair
+// of block tiles, rounds of 32 records (at most 512 queued seeds each).
+constexpr int kRecordP = 4;
+constexpr int kRecFlushR = 16;
+constexpr int kRecCapR = kRecFlushR + 64;
+constexpr int kRecRound = 32;
+constexpr int kRecQueueWords = 64 + kRecRound * 16;
+static_assert(kRecQueueWords % 4 == 0, "records start 16-byte aligned");
+static_assert(kRecQueueWords + 17 * kRecCapR + 128 + 32 <= kQCapFiltered,
+              "the record stage fits the per-wave pool");
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
 // Row and column of pair k (i <= j, row-major over the upper triangle) for
@@ -185,6 +196,14 @@ SEEDQ_INLINE uint32_t seed_of(uint32_t seedbase, int j, int h) {
 // Number of lanes below this one whose bit is set in mask.
 SEEDQ_INLINE int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0u));
+}
+
+// This lane's index, recomputed where it is used (volatile, so that it is not
+// hoisted and kept live through the walk, where registers are short).
+SEEDQ_INLINE uint32_t lane_now() {
+  uint32_t l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 
 // Queue entries: seed << 8 | final << 7 | slot (slot < 128). Seed 0 = no-op.
@@ -507,17 +526,27 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
                    int8_t* __restrict__ q_out, float* __restrict__ err_out) {
+  // At P = 4 the per-wave pool holds the candidate queue, the records (16
+  // bounds and a meta word each) and the per-slot threshold data; otherwise it
+  // is the queue alone.
+  constexpr bool kRec = P == kRecordP;
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
-  __shared__ uint32_t queue_all[kWaves][kQCapFiltered];
+  __shared__ __attribute__((aligned(16))) uint32_t pool_all[kWaves][kQCapFiltered];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // wave-uniform, so that the per-wave LDS addresses are scalar
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int n = lane & 31;   // block column of the MFMA tile
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
   unsigned long long* keys = keys_all[wave];
   int32_t* blk = blk_all[wave];
-  uint32_t* queue = queue_all[wave];
+  uint32_t* pool = pool_all[wave];
+  uint32_t* queue = pool;
+  float4 (*rec)[4] = reinterpret_cast<float4 (*)[4]>(pool + kRecQueueWords);
+  uint32_t* meta = pool + kRecQueueWords + 16 * kRecCapR;
+  float* slot_thr = reinterpret_cast<float*>(meta + kRecCapR);
+  int8_t* slot_ex = reinterpret_cast<int8_t*>(slot_thr + kSlots);
 
   int64_t begin = 0, count = nblocks;
   if (list) {
@@ -536,6 +565,25 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     if (h == 0) {
       keys[nt * 32 + n] = ~0ull;
       blk[nt * 32 + n] = int32_t(b);
+    }
+    if constexpr (kRec) {
+      if (h == 0) {
+        const bool valid = idx < count;
+        float w[kC];
+        load_block(W, b, valid, w);
+        float amax = 0.f;
+#pragma unroll
+        for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
+        const int ex = valid && amax > 0.f ? ilogbf(amax) : 0;
+        float ww = 0.f;
+#pragma unroll
+        for (int i = 0; i < kC; ++i) {
+          const float ws = ldexpf(w[i], -ex);
+          ww = fmaf(ws, ws, ww);
+        }
+        slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+        slot_ex[nt * 32 + n] = int8_t(ex);
+      }
     }
   }
   __threadfence_block();
@@ -644,7 +692,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // Evaluate the top min(64, nf) filtered entries, one per lane, until fewer
   // than min_batch remain; after any evaluation rebuild the block data and
   // thresholds. Returns whether it evaluated (wave-uniform).
-  auto exact = [&](int min_batch) __attribute__((always_inline)) {
+  auto exact_with = [&](int min_batch, auto&& rebuild) __attribute__((always_inline)) {
     bool ran = false;
     while (nf >= min_batch && nf > 0) {
       const int e = nf < 64 ? nf : 64;
@@ -683,9 +731,80 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     qcount = nf;
     if (ran) {
       __threadfence_block();
-      setup();
+      rebuild();
     }
     return ran;
+  };
+  auto exact = [&](int min_batch) __attribute__((always_inline)) { return exact_with(min_batch, setup); };
+
+  // Records -> queued seeds (P = 4): lane l < 32 takes record base + l of the
+  // top 32 and compares its 16 bounds with the block's current threshold; one
+  // ballot per seed row queues the passing seeds, and full batches are
+  // evaluated after each round, each evaluation followed at once by rebuild()
+  // (block data and the fragments the walk still needs), so that none of the
+  // walk's state is live across the evaluation.
+  int nrec = 0;  // wave-uniform
+  auto process = [&](auto&& rebuild) __attribute__((always_inline)) {
+    __threadfence_block();
+    while (nrec > 0) {
+      const int e = nrec < kRecRound ? nrec : kRecRound;
+      const int base = nrec - e;
+      uint32_t m = 0u;
+      float t = INFINITY;
+      float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0, r2 = r0, r3 = r0;
+      if (lane < e) {
+        m = meta[base + lane];
+        const int sl = int(m & 0x7Fu);
+        const unsigned long long key = keys[sl];
+        t = -INFINITY;
+        if (key != ~0ull) {
+          const double bound = key_error(key) * (1.0 + 0x1p-27);
+          t = slot_thr[sl] - __double2float_ru(ldexp(bound, 24 - 2 * int(slot_ex[sl])));
+        }
+        r0 = rec[base + lane][0];
+        r1 = rec[base + lane][1];
+        r2 = rec[base + lane][2];
+        r3 = rec[base + lane][3];
+      }
+      const float bnd[16] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w,
+                             r2.x, r2.y, r2.z, r2.w, r3.x, r3.y, r3.z, r3.w};
+      const uint32_t seedbase = (m >> 8) * 32u + 1u;
+      const int hh = int((m >> 7) & 1u);
+      const uint32_t slot = m & 0x7Fu;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool pass = bnd[j] >= t;   // t = +inf on lanes without a record
+        const uint64_t mk = ballot(pass);
+        if (mk != 0ull) {
+          if (pass) {
+            const uint32_t seed = seed_of(seedbase, j, hh);
+            queue[qcount + lanes_below(mk)] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
+          }
+          qcount += __popcll(mk);
+        }
+      }
+      nrec = base;
+      if (qcount >= 64) {
+        nf = qcount;
+        exact_with(64, rebuild);
+      }
+    }
+  };
+  // Lanes of block tile nt whose fold passed store their 16 bounds as records.
+  auto record = [&](int nt, const floatx16& acc, bool pass, uint32_t T)
+                    __attribute__((always_inline)) {
+    const uint64_t mk = ballot(pass);
+    if (mk == 0ull) return;
+    if (pass) {
+      const int r = nrec + lanes_below(mk);
+      rec[r][0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      rec[r][1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      rec[r][2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+      rec[r][3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      const uint32_t l = lane_now();   // = lane
+      meta[r] = (T << 8) | ((l >> 5) << 7) | (uint32_t(nt * 32) + (l & 31u));
+    }
+    nrec += __popcll(mk);
   };
   auto flush = [&](int min_batch) __attribute__((always_inline)) {
     filter();
@@ -792,13 +911,25 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       const bool p0 = fold_max(acc0) >= thr[0];
       const bool p1 = fold_max(acc1) >= thr[1];
       if ((ballot(p0) | ballot(p1)) != 0ull) {
-        check(I0{}, acc0, p0, seedbase);
-        check(I1{}, acc1, p1, seedbase);
-        if (qcount - nf >= 64) {
-          filter();
-          if (exact(64)) {
+        if constexpr (kRec) {
+          auto rebuild = [&]() __attribute__((always_inline)) {
+            setup();
             load_tile(T, c);
             load_tile(To, o);
+          };
+          record(0, acc0, p0, uint32_t(T));
+          if (nrec > kRecCapR - 64) process(rebuild);
+          record(1, acc1, p1, uint32_t(T));
+          if (nrec >= kRecFlushR) process(rebuild);
+        } else {
+          check(I0{}, acc0, p0, seedbase);
+          check(I1{}, acc1, p1, seedbase);
+          if (qcount - nf >= 64) {
+            filter();
+            if (exact(64)) {
+              load_tile(T, c);
+              load_tile(To, o);
+            }
           }
         }
       }
@@ -809,11 +940,22 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       const bool p2 = fold_max(acc2) >= thr[2];
       const bool p3 = fold_max(acc3) >= thr[3];
       if ((ballot(p2) | ballot(p3)) != 0ull) {
-        check(I2{}, acc2, p2, seedbase);
-        check(I3{}, acc3, p3, seedbase);
-        if (qcount - nf >= 64) {
-          filter();
-          if (exact(64)) load_tile(To, o);
+        if constexpr (kRec) {
+          auto rebuild = [&]() __attribute__((always_inline)) {
+            setup();
+            load_tile(To, o);
+          };
+          record(2, acc2, p2, uint32_t(T));
+          if (nrec > kRecCapR - 64) process(rebuild);
+          record(3, acc3, p3, uint32_t(T));
+          if (nrec >= kRecFlushR) process(rebuild);
+        } else {
+          check(I2{}, acc2, p2, seedbase);
+          check(I3{}, acc3, p3, seedbase);
+          if (qcount - nf >= 64) {
+            filter();
+            if (exact(64)) load_tile(To, o);
+          }
         }
       }
     }
@@ -828,6 +970,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     load_tile(T + 2, x);
     if (T + 1 < ntiles) tile(y, T + 1, x, T + 2);
   }
+  if constexpr (kRec) process(setup);
   flush(1);
 
   // ---------------------------------------------------------------- results
