@@ -65,8 +65,12 @@ constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane mas
 constexpr int kPilotTiles = 1;
 // P = 4 in the rebuilding kernel keeps walk survivors as records (16 bounds
 // and a meta word each) in its per-wave pool: 16 records waiting after a pair
-// of block tiles, rounds of 32 records (at most 512 queued seeds each).
+// of block tiles, rounds of 32 records (at most 512 queued seeds each). Only
+// from K = 13: with fewer seed tiles the per-wave set-up costs more than the
+// records save (measured on 2.1 M blocks: (8..10,4) 4-7 % slower, (11,4)
+// even, (12,4) 8 % slower, (13..16,4) 2.5-5 % faster, (20,4) 5 % faster).
 constexpr int kRecordP = 4;
+constexpr int kRecordMinK = 13;
 constexpr int kRecFlushR = 16;
 constexpr int kRecCapR = kRecFlushR + 64;
 constexpr int kRecRound = 32;
@@ -518,7 +522,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 // rebuilt from W, the keys and the projector stack after every evaluation
 // batch, so none of it is live across that code and the kernel fits four waves
 // per SIMD.
-template <int P>
+template <int P, bool kRec>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
 search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
@@ -526,17 +530,18 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
                    int8_t* __restrict__ q_out, float* __restrict__ err_out) {
-  // At P = 4 the per-wave pool holds the candidate queue, the records (16
-  // bounds and a meta word each) and the per-slot threshold data; otherwise it
-  // is the queue alone.
-  constexpr bool kRec = P == kRecordP;
+  // With the record stage (kRec, P = 4 only) the per-wave pool holds the
+  // candidate queue, the records (16 bounds and a meta word each) and the
+  // per-slot threshold data; otherwise it is the queue alone.
+  static_assert(!kRec || P == kRecordP, "records only at P = 4");
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
   __shared__ __attribute__((aligned(16))) uint32_t pool_all[kWaves][kQCapFiltered];
 
   const int lane = threadIdx.x & 63;
   // wave-uniform, so that the per-wave LDS addresses are scalar
-  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  // (the other variants measured faster without it)
+  const int wave = kRec ? __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6)) : int(threadIdx.x >> 6);
   const int n = lane & 31;   // block column of the MFMA tile
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
   unsigned long long* keys = keys_all[wave];
@@ -1024,12 +1029,15 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.exp_out = d_exp;
   a.q_out = d_q;
   a.err_out = d_err;
-  if constexpr (P >= 4)
-    hipLaunchKernelGGL(search_mfma_remat_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0,
+  if constexpr (P >= 4) {
+    auto kern = search_mfma_remat_kernel<P, false>;
+    if constexpr (P == kRecordP)
+      if (K >= kRecordMinK) kern = search_mfma_remat_kernel<P, true>;
+    hipLaunchKernelGGL(kern, dim3(unsigned(blocks)), dim3(kWaves * 64), 0,
                        stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
                        reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
                        a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
-  else
+  } else
     hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
                        a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
                        a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);

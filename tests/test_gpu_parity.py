@@ -125,7 +125,9 @@ def test_search_tiny_full_with_planted(sq, oq, torch):
     assert not q[:, P:].any()
 
 
-@pytest.mark.parametrize("K,P", [(8, 1), (8, 2), (9, 5), (10, 4), (10, 6), (11, 4)])
+# (13, 4) and (14, 4) take the rebuilding kernel's record stage, (10, 4) and
+# (12, 4) the per-seed checks
+@pytest.mark.parametrize("K,P", [(8, 1), (8, 2), (9, 5), (10, 4), (10, 6), (12, 4), (13, 4), (14, 4)])
 def test_search_rungs_small(sq, oq, torch, K, P):
     W = synthetic.weights(7, 8 * 37, 0.02, key=K * 16 + P, outlier_frac=0.01)   # 259 blocks: ragged
     b = sq.build_bases(K, P)
