@@ -181,6 +181,29 @@ def test_search_multi_rung_with_schedule(sq, oq, torch):
         assert not q[sel][:, P:].any()
 
 
+def test_search_every_kernel_variant_in_one_call(sq, oq, torch):
+    # one compress call whose rungs take every search variant: (10,2) the
+    # register-resident walk with records, (12,4) the rebuilding kernel's
+    # per-seed checks, (13,4) its records, (11,5) the lane-mask enqueue, (15,6)
+    # the fp32 residual filter; rungs assigned per block at random, so the
+    # compaction interleaves them arbitrarily (and leaves ragged tails)
+    rungs = ((10, 2), (12, 4), (13, 4), (11, 5), (15, 6))
+    nrows, ncols = 5, 8 * 97
+    W = synthetic.weights(nrows, ncols, 0.02, key=77, outlier_frac=0.02)
+    nb = nrows * ncols // 8
+    rob = (synthetic.splitmix64(77, synthetic.STREAM_MISC, nb) % np.uint64(len(rungs))).astype(np.uint8)
+    bases = [sq.build_bases(K, P) for K, P in rungs]
+    seed, e, q, err = sq.compress(_dev(torch, W), bases, rung_of_block=_dev(torch, rob))
+    torch.cuda.synchronize()
+    seed, e, q, err = seed.cpu().numpy().view(np.uint32), e.cpu().numpy(), q.cpu().numpy(), err.cpu().numpy()
+    blocks = W.reshape(-1, 8)
+    for r, (K, P) in enumerate(rungs):
+        sel = np.nonzero(rob == r)[0]
+        assert len(sel) > 0
+        check_search(oq, blocks[sel], K, P, seed[sel], e[sel], q[sel], err[sel], f"rung{r}")
+        assert not q[sel][:, P:].any()
+
+
 def test_invalid_rung_index_gets_seed_zero(sq, torch):
     rungs = ((8, 2), (10, 3))
     W = synthetic.weights(2, 64, 0.02, key=3)
