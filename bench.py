@@ -232,8 +232,9 @@ def main() -> int:
                     help="only time the fp16 GEMM used as the practical matrix-core reference")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
-              "blocks are independent, see DESIGN.md for how the search shards", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); blocks are "
+              "independent once the rungs are planned, so the search shards by row ranges with no "
+              "exchange beyond gathering the codes", file=sys.stderr)
         return 2
 
     import torch
