@@ -251,7 +251,8 @@ def test_search_dense_survivor_rungs(sq, oq, torch, K, P, nb):
 
 def test_search_full_size_attention_sampled(sq, oq, torch):
     # 4096 x 4096 at (16, 3), in the launch configuration the benchmark times;
-    # the oracle checks an evenly spaced sample of 192 blocks
+    # the oracle checks an evenly spaced sample of 2048 blocks and the 64 of
+    # largest magnitude
     wl = synthetic.WORKLOADS["attn4096"]
     W = synthetic.workload_weights(wl)
     K, P = wl.rungs[0]
@@ -268,8 +269,8 @@ def test_search_full_size_attention_sampled(sq, oq, torch):
     direct = (d * d).sum(axis=1)
     assert np.all(np.abs(direct - err) <= 1e-5 * direct + 1e-30)
     # outlier blocks included in the sample
-    idx = np.unique(np.concatenate([np.linspace(0, nb - 1, 160).astype(np.int64),
-                                    np.argsort(-np.abs(blocks).max(axis=1))[:32]]))
+    idx = np.unique(np.concatenate([np.linspace(0, nb - 1, 2048).astype(np.int64),
+                                    np.argsort(-np.abs(blocks).max(axis=1))[:64]]))
     check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx], "attn4096")
 
 
@@ -349,7 +350,7 @@ def test_search_full_size_three_rungs_sampled(sq, oq, torch, name):
         sel = np.nonzero(rob == r)[0]
         assert np.all((seed[sel] >= 1) & (seed[sel] < (1 << K)))
         assert not q[sel][:, P:].any()
-        n = 12 if K == 20 else 48
+        n = 64 if K == 20 else 512
         idx = sel[np.linspace(0, len(sel) - 1, n).astype(np.int64)]
         check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx],
                      f"{name} rung{r}")
