@@ -36,7 +36,9 @@
 // walk leaves free, so a second kernel rebuilds the block data and reloads the
 // seed-tile fragments after every evaluation batch instead of keeping them
 // live across it, and runs at four waves per SIMD.
+#include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <type_traits>
 
 #include "seedq_exact.h"
@@ -232,7 +234,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                   float* __restrict__ err_out) {
+                   float* __restrict__ err_out, int nsplit,
+                   unsigned long long* __restrict__ split_keys) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
   __shared__ float thr_base_all[kWaves][kSlots];   // ||w||^2 (1 - gamma) in accumulator units
@@ -470,10 +473,13 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // loaded while the other tile is screened. The loads are unconditional (the
   // index is clamped to the last tile) so that the wait before each tile
   // covers only that tile's own loads.
-  const int64_t last = ntiles - 1;
-  half8 x0 = A[lane], x1 = A[64 + lane], x2 = A[128 + lane];
+  // Seed split blockIdx.y walks tiles [T0, T1) (at least 8 of them).
+  const int64_t T0 = int64_t(blockIdx.y) * ntiles / nsplit;
+  const int64_t T1 = int64_t(blockIdx.y + 1) * ntiles / nsplit;
+  const int64_t last = T1 - 1;
+  half8 x0 = A[T0 * 192 + lane], x1 = A[T0 * 192 + 64 + lane], x2 = A[T0 * 192 + 128 + lane];
   half8 y0, y1, y2;
-  for (int64_t T = 0; T < ntiles; T += 2) {
+  for (int64_t T = T0; T < T1; T += 2) {
     {
       const half8* An = A + (T + 1 < last ? T + 1 : last) * 192;
       y0 = An[lane];
@@ -487,12 +493,20 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       x1 = An[64 + lane];
       x2 = An[128 + lane];
     }
-    if (T + 1 < ntiles) tile(y0, y1, y2, T + 1);
+    if (T + 1 < T1) tile(y0, y1, y2, T + 1);
   }
   process();
   evaluate(1);
 
   // ---------------------------------------------------------------- results
+  // A seed split only folds its best keys into the global ones; the codes are
+  // emitted once all splits are done.
+  if (split_keys) {
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt)
+      if (h == 0 && active[nt]) atomicMin(&split_keys[blk[nt * 32 + n]], keys[nt * 32 + n]);
+    return;
+  }
   // the winning seed of every block, evaluated once more to emit its code
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
@@ -529,7 +543,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const double* __restrict__ pinv64, const float* __restrict__ q32,
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
-                   int8_t* __restrict__ q_out, float* __restrict__ err_out) {
+                   int8_t* __restrict__ q_out, float* __restrict__ err_out, int nsplit,
+                   unsigned long long* __restrict__ split_keys) {
   // With the record stage (kRec, P = 4 only) the per-wave pool holds the
   // candidate queue, the records (16 bounds and a meta word each) and the
   // per-slot threshold data; otherwise it is the queue alone.
@@ -895,7 +910,10 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 
   // Seed-tile fragments; the index is clamped to the last tile so that every
   // load is unconditional and each wait covers only the tile it is for.
-  const int64_t last = ntiles - 1;
+  // Seed split blockIdx.y walks tiles [T0, T1) (at least 8 of them).
+  const int64_t T0 = int64_t(blockIdx.y) * ntiles / nsplit;
+  const int64_t T1 = int64_t(blockIdx.y + 1) * ntiles / nsplit;
+  const int64_t last = T1 - 1;
   auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
     const half8* At = A + (T < last ? T : last) * 192;
     f[0] = At[lane];
@@ -968,17 +986,27 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 
   // Two fragment sets in turn: one tile is loaded while the other is screened.
   half8 x[3], y[3];
-  load_tile(0, x);
-  for (int64_t T = 0; T < ntiles; T += 2) {
+  load_tile(T0, x);
+  for (int64_t T = T0; T < T1; T += 2) {
     load_tile(T + 1, y);
     tile(x, T, y, T + 1);
     load_tile(T + 2, x);
-    if (T + 1 < ntiles) tile(y, T + 1, x, T + 2);
+    if (T + 1 < T1) tile(y, T + 1, x, T + 2);
   }
   if constexpr (kRec) process(setup);
   flush(1);
 
   // ---------------------------------------------------------------- results
+  // A seed split only folds its best keys into the global ones.
+  if (split_keys) {
+#pragma unroll
+    for (int nt = 0; nt < kNB; ++nt) {
+      const unsigned long long key = keys[nt * 32 + n];
+      if (h == 0 && wave_base + nt * 32 + n < count && key != ~0ull)
+        atomicMin(&split_keys[blk[nt * 32 + n]], key);
+    }
+    return;
+  }
   // The winning seed of every block, evaluated once more to emit its code.
   // Every searched block holds a key after the pilot; a valid block without
   // one is all zero, where every seed ties and the smallest wins.
@@ -1001,6 +1029,77 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     }
   }
   flush(1);
+}
+
+// ---------------------------------------------------------------- seed splits
+// A uniform-rung search of too few blocks to fill the GPU walks the seed tiles
+// in nsplit ranges (grid dimension y), each range a separate wave per block
+// tile. The per-block keys of all ranges meet in a global minimum held in the
+// caller's mantissa output (8 bytes per block, 8-byte aligned): keys order
+// candidates by (error to 2^-28, seed) and every range evaluates exactly what
+// could still win within it, so the minimum over ranges is the key the
+// unsplit search ends with. A last pass emits each block's code from it.
+
+__global__ void __launch_bounds__(256)
+split_init_kernel(unsigned long long* __restrict__ keys, int64_t nblocks) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i < nblocks) keys[i] = ~0ull;
+}
+
+template <int P>
+__global__ void __launch_bounds__(256)
+split_emit_kernel(const float* __restrict__ W, int64_t nblocks, int K, uint32_t mask,
+                  const double* __restrict__ pinv64, uint32_t* __restrict__ seed_out,
+                  uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
+                  float* __restrict__ err_out) {
+  const int64_t b = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (b >= nblocks) return;
+  float w[kC];
+  load_block(W, b, true, w);
+  float amax = 0.f;
+#pragma unroll
+  for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
+  uint2* qw = reinterpret_cast<uint2*>(q_out);
+  if (amax == 0.f) {
+    // all-zero block: every seed ties, the smallest one wins
+    seed_out[b] = 1u;
+    exp_out[b] = 15;
+    qw[b] = make_uint2(0u, 0u);
+    if (err_out) err_out[b] = 0.f;
+    return;
+  }
+  const unsigned long long key = reinterpret_cast<const unsigned long long*>(q_out)[b];
+  // every searched block holds a key after the pilot; seed 1 is a guard
+  const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
+  int qe, q[P];
+  const double err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+  seed_out[b] = seed;
+  exp_out[b] = uint8_t(qe);
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
+    if (p < 4) lo |= byte << (8 * p);
+    else hi |= byte << (8 * (p - 4));
+  }
+  qw[b] = make_uint2(lo, hi);
+  if (err_out) err_out[b] = float(err);
+}
+
+// Number of seed ranges for a uniform-rung search of nblocks blocks: enough
+// waves for two per wave slot (1024 SIMDs at the kernel's occupancy), at most
+// 256 ranges and at least 8 seed tiles per range. SEEDQ_SEED_SPLITS overrides
+// the choice (clamped to the same limits).
+int seed_splits(int64_t nblocks, int64_t ntiles, int waves_per_simd) {
+  const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(256, ntiles / 8));
+  if (const char* env = std::getenv("SEEDQ_SEED_SPLITS")) {
+    const long v = std::strtol(env, nullptr, 10);
+    if (v >= 1) return int(std::min<int64_t>(v, smax));
+  }
+  const int64_t waves = (nblocks + kSlots - 1) / kSlots;
+  const int64_t want = 2 * 1024 * int64_t(waves_per_simd);
+  if (waves >= want) return 1;
+  return int(std::min<int64_t>(smax, (want + waves - 1) / waves));
 }
 
 template <int P>
@@ -1029,18 +1128,32 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.exp_out = d_exp;
   a.q_out = d_q;
   a.err_out = d_err;
+  // seed ranges only for a uniform-rung search (its block count is known here)
+  const int nsplit = d_list ? 1 : seed_splits(nblocks, L.ntiles, P >= 4 ? 4 : 3);
+  unsigned long long* keys = nullptr;
+  const unsigned nb256 = unsigned((nblocks + 255) / 256);
+  if (nsplit > 1) {
+    keys = reinterpret_cast<unsigned long long*>(d_q);
+    hipLaunchKernelGGL(split_init_kernel, dim3(nb256), dim3(256), 0, stream, keys, nblocks);
+  }
+  const dim3 grid = dim3(unsigned(blocks), unsigned(nsplit), 1u);
   if constexpr (P >= 4) {
     auto kern = search_mfma_remat_kernel<P, false>;
     if constexpr (P == kRecordP)
       if (K >= kRecordMinK) kern = search_mfma_remat_kernel<P, true>;
-    hipLaunchKernelGGL(kern, dim3(unsigned(blocks)), dim3(kWaves * 64), 0,
+    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0,
                        stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
                        reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
-                       a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
-  } else
-    hipLaunchKernelGGL(search_mfma_kernel<P>, dim3(unsigned(blocks)), dim3(kWaves * 64), 0, stream,
+                       a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, nsplit, keys);
+  } else {
+    hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
                        a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
-                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out);
+                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
+                       nsplit, keys);
+  }
+  if (nsplit > 1)
+    hipLaunchKernelGGL(split_emit_kernel<P>, dim3(nb256), dim3(256), 0, stream, a.W, nblocks, a.K,
+                       a.mask, a.pinv64, a.seed_out, a.exp_out, a.q_out, a.err_out);
   return hipGetLastError();
 }
 

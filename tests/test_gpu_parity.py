@@ -215,6 +215,35 @@ def test_invalid_rung_index_gets_seed_zero(sq, torch):
     assert np.all((seed == 0) == (rob >= 2))
 
 
+@pytest.mark.parametrize("K,P", [(12, 3), (14, 2), (16, 3), (13, 4), (12, 4), (11, 5), (15, 6)])
+def test_search_seed_splits_match_unsplit(sq, torch, K, P):
+    # a uniform-rung search of few blocks walks the seed range in several parts
+    # whose per-block keys meet in a global minimum; every split must give the
+    # unsplit codes bit for bit (including all-zero blocks and a ragged tail)
+    import os
+    W = synthetic.weights(3, 8 * 203, 0.02, key=90 + K + P, outlier_frac=0.02)
+    W[1, 8 * 5:8 * 6] = 0.0
+    b = sq.build_bases(K, P)
+    d = _dev(torch, W)
+    out = {}
+    old = os.environ.get("SEEDQ_SEED_SPLITS")
+    try:
+        for splits in ("1", "2", "7", None):
+            if splits is None:
+                os.environ.pop("SEEDQ_SEED_SPLITS", None)   # the library's own choice
+            else:
+                os.environ["SEEDQ_SEED_SPLITS"] = splits
+            out[splits] = [t.cpu() for t in sq.compress(d, [b])]
+    finally:
+        if old is None:
+            os.environ.pop("SEEDQ_SEED_SPLITS", None)
+        else:
+            os.environ["SEEDQ_SEED_SPLITS"] = old
+    for splits in ("2", "7", None):
+        for a, c in zip(out["1"], out[splits]):
+            assert torch.equal(a, c), (K, P, splits)
+
+
 def test_search_deterministic(sq, torch):
     W = synthetic.weights(32, 256, 0.02, key=8, outlier_frac=0.001)
     b = sq.build_bases(12, 3)
