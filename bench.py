@@ -107,11 +107,18 @@ def cpu_baseline(W: np.ndarray, K: int, P: int, target_s: float = 15.0) -> dict:
     oracle.search(sample, K, P, threads=threads, pinv=pinv)
     dt = time.perf_counter() - t0
     cands = n * ((1 << K) - 1)
+    # the same oracle on one thread, over a smaller evenly spaced sample (~3 s)
+    n1 = int(min(len(blocks), max(4, 3.0 * rate / threads / ((1 << K) - 1))))
+    s1 = np.ascontiguousarray(blocks[np.linspace(0, len(blocks) - 1, n1).astype(np.int64)])
+    t0 = time.perf_counter()
+    oracle.search(s1, K, P, threads=1, pinv=pinv)
+    rate1 = n1 * ((1 << K) - 1) / (time.perf_counter() - t0)
     return {"value": cands / dt, "unit": "block·seed candidates/s", "cores": int(threads),
+            "value_one_thread": rate1,
             "kind": "oracle",
             "sample": f"{n} evenly spaced blocks of the same matrix at (K={K}, P={P}), "
-                      f"{cands:.3g} candidates in {dt:.1f} s; per-seed pseudo-inverses "
-                      f"precomputed outside the timed region"}
+                      f"{cands:.3g} candidates in {dt:.1f} s; one thread: {n1} blocks; per-seed "
+                      f"pseudo-inverses precomputed outside the timed region"}
 
 
 def decoder_bench(args) -> int:
