@@ -234,7 +234,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                   float* __restrict__ err_out, int nsplit,
+                   float* __restrict__ err_out, int nsplit, int split0,
                    unsigned long long* __restrict__ split_keys) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
@@ -293,7 +293,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     bop[nt][1] = b_fragment<1>(ws, h);
     bop[nt][2] = b_fragment<2>(ws, h);
     if (h == 0) {
-      keys[nt * 32 + n] = ~0ull;
+      // a later launch of a sequential range split starts from the best so far
+      keys[nt * 32 + n] = split0 > 0 && valid[nt] ? split_keys[b] : ~0ull;
       blk[nt * 32 + n] = int32_t(b);
       // thresholds live in accumulator units (both operands carry 2^12)
       slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
@@ -408,8 +409,11 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // ---------------------------------------------------------------- pilot
   // Over the first tile each lane tracks its seed of smallest bound; their
   // exact errors start every block's best. (Longer pilots cost more matrix
-  // time than the survivors they save.)
-  {
+  // time than the survivors they save.) Later launches of a sequential range
+  // split start from the keys instead.
+  if (split0 > 0) {
+    refresh();
+  } else {
     const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
@@ -473,9 +477,10 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // loaded while the other tile is screened. The loads are unconditional (the
   // index is clamped to the last tile) so that the wait before each tile
   // covers only that tile's own loads.
-  // Seed split blockIdx.y walks tiles [T0, T1) (at least 8 of them).
-  const int64_t T0 = int64_t(blockIdx.y) * ntiles / nsplit;
-  const int64_t T1 = int64_t(blockIdx.y + 1) * ntiles / nsplit;
+  // Seed range split0 + blockIdx.y walks tiles [T0, T1) (at least 8 of them).
+  const int64_t rng = int64_t(split0) + blockIdx.y;
+  const int64_t T0 = rng * ntiles / nsplit;
+  const int64_t T1 = (rng + 1) * ntiles / nsplit;
   const int64_t last = T1 - 1;
   half8 x0 = A[T0 * 192 + lane], x1 = A[T0 * 192 + 64 + lane], x2 = A[T0 * 192 + 128 + lane];
   half8 y0, y1, y2;
@@ -544,7 +549,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
                    int8_t* __restrict__ q_out, float* __restrict__ err_out, int nsplit,
-                   unsigned long long* __restrict__ split_keys) {
+                   int split0, unsigned long long* __restrict__ split_keys) {
   // With the record stage (kRec, P = 4 only) the per-wave pool holds the
   // candidate queue, the records (16 bounds and a meta word each) and the
   // per-slot threshold data; otherwise it is the queue alone.
@@ -583,7 +588,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     const int64_t idx = wave_base + nt * 32 + n;
     const int64_t b = idx < count ? (list ? int64_t(list[begin + idx]) : idx) : 0;
     if (h == 0) {
-      keys[nt * 32 + n] = ~0ull;
+      // a later launch of a sequential range split starts from the best so far
+      keys[nt * 32 + n] = split0 > 0 && idx < count ? split_keys[b] : ~0ull;
       blk[nt * 32 + n] = int32_t(b);
     }
     if constexpr (kRec) {
@@ -837,8 +843,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // ---------------------------------------------------------------- pilot
   // Over the first tile each lane takes its seed of smallest bound; their exact
   // errors start every block's best. (Longer pilots cost more matrix time than
-  // the survivors they save.)
-  {
+  // the survivors they save.) Later launches of a sequential range split start
+  // from the keys (setup() above has turned them into thresholds).
+  if (split0 == 0) {
     const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
@@ -910,9 +917,10 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 
   // Seed-tile fragments; the index is clamped to the last tile so that every
   // load is unconditional and each wait covers only the tile it is for.
-  // Seed split blockIdx.y walks tiles [T0, T1) (at least 8 of them).
-  const int64_t T0 = int64_t(blockIdx.y) * ntiles / nsplit;
-  const int64_t T1 = int64_t(blockIdx.y + 1) * ntiles / nsplit;
+  // Seed range split0 + blockIdx.y walks tiles [T0, T1) (at least 8 of them).
+  const int64_t rng = int64_t(split0) + blockIdx.y;
+  const int64_t T0 = rng * ntiles / nsplit;
+  const int64_t T1 = (rng + 1) * ntiles / nsplit;
   const int64_t last = T1 - 1;
   auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
     const half8* At = A + (T < last ? T : last) * 192;
@@ -1031,29 +1039,49 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   flush(1);
 }
 
-// ---------------------------------------------------------------- seed splits
-// A uniform-rung search of too few blocks to fill the GPU walks the seed tiles
-// in nsplit ranges (grid dimension y), each range a separate wave per block
-// tile. The per-block keys of all ranges meet in a global minimum held in the
-// caller's mantissa output (8 bytes per block, 8-byte aligned): keys order
-// candidates by (error to 2^-28, seed) and every range evaluates exactly what
-// could still win within it, so the minimum over ranges is the key the
-// unsplit search ends with. A last pass emits each block's code from it.
+// ---------------------------------------------------------------- seed ranges
+// The seed tiles of a rung can be walked in nsplit ranges: in sequence, one
+// launch per chunk of kChunkTiles tiles, so that every wave walks the same 6 MB
+// of projector fragments at about the same time and they stay in L2 (one walk
+// over a 101 MB stack at K = 20 missed L2 on most requests); and, for a
+// uniform-rung search too small to fill the GPU, several ranges at once (grid
+// dimension y). The per-block keys of all ranges meet in a global minimum held
+// in the caller's mantissa output (8 bytes per block, 8-byte aligned); a later
+// launch starts from it, so the thresholds carry over and only the first one
+// runs the pilot. Keys order candidates by (error to 2^-28, seed) and every
+// range evaluates whatever could still win within it, so the final minimum is
+// the key the unsplit search ends with. A last pass emits each block's code.
+constexpr int64_t kChunkTiles = 2048;
+
+__device__ __forceinline__ bool rung_block(const int32_t* list, const int32_t* off, int rung,
+                                           int64_t nblocks, int64_t i, int64_t& b) {
+  int64_t begin = 0, count = nblocks;
+  if (list) {
+    begin = off[rung];
+    count = int64_t(off[rung + 1]) - begin;
+  }
+  if (i >= count) return false;
+  b = list ? int64_t(list[begin + i]) : i;
+  return true;
+}
 
 __global__ void __launch_bounds__(256)
-split_init_kernel(unsigned long long* __restrict__ keys, int64_t nblocks) {
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i < nblocks) keys[i] = ~0ull;
+split_init_kernel(unsigned long long* __restrict__ keys, int64_t nblocks,
+                  const int32_t* __restrict__ list, const int32_t* __restrict__ off, int rung) {
+  int64_t b;
+  if (rung_block(list, off, rung, nblocks, int64_t(blockIdx.x) * 256 + threadIdx.x, b))
+    keys[b] = ~0ull;
 }
 
 template <int P>
 __global__ void __launch_bounds__(256)
-split_emit_kernel(const float* __restrict__ W, int64_t nblocks, int K, uint32_t mask,
+split_emit_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
+                  const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
                   const double* __restrict__ pinv64, uint32_t* __restrict__ seed_out,
                   uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
                   float* __restrict__ err_out) {
-  const int64_t b = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (b >= nblocks) return;
+  int64_t b;
+  if (!rung_block(list, off, rung, nblocks, int64_t(blockIdx.x) * 256 + threadIdx.x, b)) return;
   float w[kC];
   load_block(W, b, true, w);
   float amax = 0.f;
@@ -1086,16 +1114,23 @@ split_emit_kernel(const float* __restrict__ W, int64_t nblocks, int K, uint32_t 
   if (err_out) err_out[b] = float(err);
 }
 
-// Number of seed ranges for a uniform-rung search of nblocks blocks: enough
-// waves for two per wave slot (1024 SIMDs at the kernel's occupancy), at most
-// 256 ranges and at least 8 seed tiles per range. SEEDQ_SEED_SPLITS overrides
-// the choice (clamped to the same limits).
+int64_t env_int(const char* name, int64_t fallback) {
+  if (const char* env = std::getenv(name)) {
+    char* end = nullptr;
+    const long long v = std::strtoll(env, &end, 10);
+    if (end != env && v >= 0) return v;
+  }
+  return fallback;
+}
+
+// Number of concurrent ranges for a uniform-rung search of nblocks blocks over
+// ntiles tiles: enough waves for two per wave slot (1024 SIMDs at the kernel's
+// occupancy), at most 256 ranges and at least 8 seed tiles per range.
+// SEEDQ_SEED_SPLITS overrides the choice (clamped to the same limits).
 int seed_splits(int64_t nblocks, int64_t ntiles, int waves_per_simd) {
   const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(256, ntiles / 8));
-  if (const char* env = std::getenv("SEEDQ_SEED_SPLITS")) {
-    const long v = std::strtol(env, nullptr, 10);
-    if (v >= 1) return int(std::min<int64_t>(v, smax));
-  }
+  const int64_t forced = env_int("SEEDQ_SEED_SPLITS", 0);
+  if (forced >= 1) return int(std::min<int64_t>(forced, smax));
   const int64_t waves = (nblocks + kSlots - 1) / kSlots;
   const int64_t want = 2 * 1024 * int64_t(waves_per_simd);
   if (waves >= want) return 1;
@@ -1128,32 +1163,43 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.exp_out = d_exp;
   a.q_out = d_q;
   a.err_out = d_err;
-  // seed ranges only for a uniform-rung search (its block count is known here)
-  const int nsplit = d_list ? 1 : seed_splits(nblocks, L.ntiles, P >= 4 ? 4 : 3);
+  // sequential chunks of the seed tiles (SEEDQ_SEED_CHUNK_TILES overrides the
+  // chunk length; 0 = one chunk), then concurrent ranges within each chunk for
+  // a uniform-rung search (its block count is known here)
+  const int64_t chunk = env_int("SEEDQ_SEED_CHUNK_TILES", kChunkTiles);
+  const int64_t nseq = chunk > 0 ? std::max<int64_t>(1, std::min<int64_t>(L.ntiles / 8, L.ntiles / chunk)) : 1;
+  const int nconc = d_list ? 1 : seed_splits(nblocks, L.ntiles / nseq, P >= 4 ? 4 : 3);
+  const int nsplit = int(nseq) * nconc;
   unsigned long long* keys = nullptr;
   const unsigned nb256 = unsigned((nblocks + 255) / 256);
   if (nsplit > 1) {
     keys = reinterpret_cast<unsigned long long*>(d_q);
-    hipLaunchKernelGGL(split_init_kernel, dim3(nb256), dim3(256), 0, stream, keys, nblocks);
+    hipLaunchKernelGGL(split_init_kernel, dim3(nb256), dim3(256), 0, stream, keys, nblocks, a.list,
+                       a.off, a.rung);
   }
-  const dim3 grid = dim3(unsigned(blocks), unsigned(nsplit), 1u);
-  if constexpr (P >= 4) {
-    auto kern = search_mfma_remat_kernel<P, false>;
-    if constexpr (P == kRecordP)
-      if (K >= kRecordMinK) kern = search_mfma_remat_kernel<P, true>;
-    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0,
-                       stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
-                       reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
-                       a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, nsplit, keys);
-  } else {
-    hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
-                       a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
-                       a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
-                       nsplit, keys);
+  const dim3 grid = dim3(unsigned(blocks), unsigned(nconc), 1u);
+  for (int64_t c = 0; c < nseq; ++c) {
+    const int split0 = int(c) * nconc;
+    if constexpr (P >= 4) {
+      auto kern = search_mfma_remat_kernel<P, false>;
+      if constexpr (P == kRecordP)
+        if (K >= kRecordMinK) kern = search_mfma_remat_kernel<P, true>;
+      hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0,
+                         stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
+                         reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
+                         a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, nsplit,
+                         split0, keys);
+    } else {
+      hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
+                         a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
+                         a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
+                         nsplit, split0, keys);
+    }
   }
   if (nsplit > 1)
-    hipLaunchKernelGGL(split_emit_kernel<P>, dim3(nb256), dim3(256), 0, stream, a.W, nblocks, a.K,
-                       a.mask, a.pinv64, a.seed_out, a.exp_out, a.q_out, a.err_out);
+    hipLaunchKernelGGL(split_emit_kernel<P>, dim3(nb256), dim3(256), 0, stream, a.W, nblocks,
+                       a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.seed_out, a.exp_out, a.q_out,
+                       a.err_out);
   return hipGetLastError();
 }
 

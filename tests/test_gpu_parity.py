@@ -215,33 +215,41 @@ def test_invalid_rung_index_gets_seed_zero(sq, torch):
     assert np.all((seed == 0) == (rob >= 2))
 
 
-@pytest.mark.parametrize("K,P", [(12, 3), (14, 2), (16, 3), (13, 4), (12, 4), (11, 5), (15, 6)])
+@pytest.mark.parametrize("K,P", [(12, 3), (14, 2), (16, 3), (13, 4), (12, 4), (11, 5), (15, 6),
+                                 (17, 3), (18, 4)])
 def test_search_seed_splits_match_unsplit(sq, torch, K, P):
-    # a uniform-rung search of few blocks walks the seed range in several parts
-    # whose per-block keys meet in a global minimum; every split must give the
-    # unsplit codes bit for bit (including all-zero blocks and a ragged tail)
+    # the seed tiles walked in ranges -- sequential chunks of SEEDQ_SEED_CHUNK_TILES
+    # tiles (2048 by default, so K >= 17 is chunked) and, for a uniform-rung
+    # search of few blocks, concurrent ranges -- whose per-block keys meet in a
+    # global minimum; every split must give the single walk's codes bit for bit
+    # (including an all-zero block and a ragged tail)
     import os
     W = synthetic.weights(3, 8 * 203, 0.02, key=90 + K + P, outlier_frac=0.02)
     W[1, 8 * 5:8 * 6] = 0.0
     b = sq.build_bases(K, P)
     d = _dev(torch, W)
+    names = ("SEEDQ_SEED_CHUNK_TILES", "SEEDQ_SEED_SPLITS")
+    saved = {n: os.environ.get(n) for n in names}
+    cases = {"single walk": ("0", "1"), "default": (None, None), "chunks of 64": ("64", "1"),
+             "chunks of 256, 3 at once": ("256", "3"), "one chunk, 7 at once": ("0", "7")}
     out = {}
-    old = os.environ.get("SEEDQ_SEED_SPLITS")
     try:
-        for splits in ("1", "2", "7", None):
-            if splits is None:
-                os.environ.pop("SEEDQ_SEED_SPLITS", None)   # the library's own choice
-            else:
-                os.environ["SEEDQ_SEED_SPLITS"] = splits
-            out[splits] = [t.cpu() for t in sq.compress(d, [b])]
+        for label, vals in cases.items():
+            for n, v in zip(names, vals):
+                if v is None:
+                    os.environ.pop(n, None)
+                else:
+                    os.environ[n] = v
+            out[label] = [t.cpu() for t in sq.compress(d, [b])]
     finally:
-        if old is None:
-            os.environ.pop("SEEDQ_SEED_SPLITS", None)
-        else:
-            os.environ["SEEDQ_SEED_SPLITS"] = old
-    for splits in ("2", "7", None):
-        for a, c in zip(out["1"], out[splits]):
-            assert torch.equal(a, c), (K, P, splits)
+        for n, v in saved.items():
+            if v is None:
+                os.environ.pop(n, None)
+            else:
+                os.environ[n] = v
+    for label in cases:
+        for a, c in zip(out["single walk"], out[label]):
+            assert torch.equal(a, c), (K, P, label)
 
 
 def test_search_deterministic(sq, torch):
