@@ -27,8 +27,10 @@
 // infinite threshold. The final codes go through the same queue.
 //
 // Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
-// blocks (128 blocks) and walks all seed tiles once, reusing each A fragment
+// blocks (128 blocks) and walks the seed tiles once, reusing each A fragment
 // for its 4 block tiles; its B fragments stay in registers for the whole walk.
+// Large rungs walk the seed tiles in sequential chunks and small uniform
+// searches in concurrent ranges (see "seed ranges" below).
 // Block tiles go to the matrix core in pairs (six products) before the vector
 // ALU folds them, with one branch per pair; the fold waits on its own
 // products, so it is occupancy (several waves per SIMD) that keeps the matrix
@@ -53,7 +55,6 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
-constexpr int kQCap = 64 + 2 * 1024; // survivor queue entries per wave
 // With the residual filter up to 63 filtered and 63 new entries wait before a
 // pair of block tiles adds its at most 2 x 1024.
 constexpr int kQCapFiltered = 128 + 2 * 1024;
