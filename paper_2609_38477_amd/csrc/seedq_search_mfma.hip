@@ -55,8 +55,9 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
-// With the residual filter up to 63 filtered and 63 new entries wait before a
-// pair of block tiles adds its at most 2 x 1024.
+// Queue entries per wave of the rebuilding kernel: with the residual filter up
+// to 63 filtered and 63 new entries wait before a pair of block tiles adds its
+// at most 2 x 1024.
 constexpr int kQCapFiltered = 128 + 2 * 1024;
 // Rungs that use the residual filter: it defers exact evaluations until 64
 // filtered entries wait, which pays only where most survivors of the matrix
@@ -65,7 +66,6 @@ constexpr int kQCapFiltered = 128 + 2 * 1024;
 constexpr int kFilterMinP = 6;
 constexpr int kFilterMinK = 15;
 constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane masks
-constexpr int kPilotTiles = 1;
 // P = 4 in the rebuilding kernel keeps walk survivors as records (16 bounds
 // and a meta word each) in its per-wave pool: 16 records waiting after a pair
 // of block tiles, rounds of 32 records (at most 512 queued seeds each). Only
