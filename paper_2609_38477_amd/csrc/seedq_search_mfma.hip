@@ -438,9 +438,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 
   // ---------------------------------------------------------------- seed walk
   // Lanes of block tile nt whose fold passed store their 16 bounds as records.
-  auto record = [&](int nt, const floatx16& acc, bool pass, uint32_t T)
+  // mk = ballot(pass), taken once by the caller.
+  auto record = [&](int nt, const floatx16& acc, bool pass, uint64_t mk, uint32_t T)
                     __attribute__((always_inline)) {
-    const uint64_t mk = ballot(pass);
     if (mk == 0ull) return;
     if (pass) {
       const int r = nrec + lanes_below(mk);
@@ -466,10 +466,11 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       const floatx16 acc1 = bounds(a0, a1, a2, bop[2 * pr + 1]);
       const bool p0 = fold_max(acc0) >= thr[2 * pr];
       const bool p1 = fold_max(acc1) >= thr[2 * pr + 1];
-      if ((ballot(p0) | ballot(p1)) != 0ull) {
-        record(2 * pr, acc0, p0, t32);
+      const uint64_t m0 = ballot(p0), m1 = ballot(p1);
+      if ((m0 | m1) != 0ull) {
+        record(2 * pr, acc0, p0, m0, t32);
         if (nrec > kRecCap - 64) process();
-        record(2 * pr + 1, acc1, p1, t32);
+        record(2 * pr + 1, acc1, p1, m1, t32);
         if (nrec >= kRecFlush) process();
       }
     }
@@ -818,9 +819,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     }
   };
   // Lanes of block tile nt whose fold passed store their 16 bounds as records.
-  auto record = [&](int nt, const floatx16& acc, bool pass, uint32_t T)
+  // mk = ballot(pass), taken once by the caller.
+  auto record = [&](int nt, const floatx16& acc, bool pass, uint64_t mk, uint32_t T)
                     __attribute__((always_inline)) {
-    const uint64_t mk = ballot(pass);
     if (mk == 0ull) return;
     if (pass) {
       const int r = nrec + lanes_below(mk);
@@ -942,16 +943,17 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       const floatx16 acc1 = bounds(c[0], c[1], c[2], bop[1]);
       const bool p0 = fold_max(acc0) >= thr[0];
       const bool p1 = fold_max(acc1) >= thr[1];
-      if ((ballot(p0) | ballot(p1)) != 0ull) {
+      const uint64_t m0 = ballot(p0), m1 = ballot(p1);
+      if ((m0 | m1) != 0ull) {
         if constexpr (kRec) {
           auto rebuild = [&]() __attribute__((always_inline)) {
             setup();
             load_tile(T, c);
             load_tile(To, o);
           };
-          record(0, acc0, p0, uint32_t(T));
+          record(0, acc0, p0, m0, uint32_t(T));
           if (nrec > kRecCapR - 64) process(rebuild);
-          record(1, acc1, p1, uint32_t(T));
+          record(1, acc1, p1, m1, uint32_t(T));
           if (nrec >= kRecFlushR) process(rebuild);
         } else {
           check(I0{}, acc0, p0, seedbase);
@@ -971,15 +973,16 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       const floatx16 acc3 = bounds(c[0], c[1], c[2], bop[3]);
       const bool p2 = fold_max(acc2) >= thr[2];
       const bool p3 = fold_max(acc3) >= thr[3];
-      if ((ballot(p2) | ballot(p3)) != 0ull) {
+      const uint64_t m2 = ballot(p2), m3 = ballot(p3);
+      if ((m2 | m3) != 0ull) {
         if constexpr (kRec) {
           auto rebuild = [&]() __attribute__((always_inline)) {
             setup();
             load_tile(To, o);
           };
-          record(2, acc2, p2, uint32_t(T));
+          record(2, acc2, p2, m2, uint32_t(T));
           if (nrec > kRecCapR - 64) process(rebuild);
-          record(3, acc3, p3, uint32_t(T));
+          record(3, acc3, p3, m3, uint32_t(T));
           if (nrec >= kRecFlushR) process(rebuild);
         } else {
           check(I2{}, acc2, p2, seedbase);
