@@ -213,6 +213,19 @@ SEEDQ_INLINE uint32_t lane_now() {
   return l;
 }
 
+// Concurrent seed ranges of a launch: nconc_arg > 0 is the number itself;
+// nconc_arg < 0 lets the launch choose, from its rung's block count, enough
+// ranges for two waves per wave slot (1024 SIMDs at waves_per_simd), at most
+// -nconc_arg. Wave-uniform; count >= 1.
+__device__ __forceinline__ int concurrent_ranges(int nconc_arg, int64_t count, int waves_per_simd) {
+  if (nconc_arg > 0) return nconc_arg;
+  const int64_t waves = (count + kSlots - 1) / kSlots;
+  const int64_t want = 2 * 1024 * int64_t(waves_per_simd);
+  if (waves >= want) return 1;
+  const int64_t n = (want + waves - 1) / waves;
+  return int(n < -nconc_arg ? n : -nconc_arg);
+}
+
 // Queue entries: seed << 8 | final << 7 | slot (slot < 128). Seed 0 = no-op.
 constexpr uint32_t kFinal = 0x80u;
 static_assert(kSlots <= 128, "slot must fit 7 bits");
@@ -235,7 +248,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                   float* __restrict__ err_out, int nsplit, int split0,
+                   float* __restrict__ err_out, int nchunks, int chunk, int nconc_arg,
                    unsigned long long* __restrict__ split_keys) {
   __shared__ unsigned long long keys_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
@@ -265,6 +278,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   }
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
+  const int nconc = concurrent_ranges(nconc_arg, count, 3);
+  if (int(blockIdx.y) >= nconc) return;  // a range this rung does not need
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
 
   // ---------------------------------------------------------------- prologue
@@ -295,7 +310,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     bop[nt][2] = b_fragment<2>(ws, h);
     if (h == 0) {
       // a later launch of a sequential range split starts from the best so far
-      keys[nt * 32 + n] = split0 > 0 && valid[nt] ? split_keys[b] : ~0ull;
+      keys[nt * 32 + n] = chunk > 0 && valid[nt] ? split_keys[b] : ~0ull;
       blk[nt * 32 + n] = int32_t(b);
       // thresholds live in accumulator units (both operands carry 2^12)
       slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
@@ -412,7 +427,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // exact errors start every block's best. (Longer pilots cost more matrix
   // time than the survivors they save.) Later launches of a sequential range
   // split start from the keys instead.
-  if (split0 > 0) {
+  if (chunk > 0) {
     refresh();
   } else {
     const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
@@ -479,10 +494,10 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // loaded while the other tile is screened. The loads are unconditional (the
   // index is clamped to the last tile) so that the wait before each tile
   // covers only that tile's own loads.
-  // Seed range split0 + blockIdx.y walks tiles [T0, T1) (at least 8 of them).
-  const int64_t rng = int64_t(split0) + blockIdx.y;
-  const int64_t T0 = rng * ntiles / nsplit;
-  const int64_t T1 = (rng + 1) * ntiles / nsplit;
+  // Range blockIdx.y of chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
+  const int64_t C0 = int64_t(chunk) * ntiles / nchunks, C1 = int64_t(chunk + 1) * ntiles / nchunks;
+  const int64_t T0 = C0 + int64_t(blockIdx.y) * (C1 - C0) / nconc;
+  const int64_t T1 = C0 + int64_t(blockIdx.y + 1) * (C1 - C0) / nconc;
   const int64_t last = T1 - 1;
   half8 x0 = A[T0 * 192 + lane], x1 = A[T0 * 192 + 64 + lane], x2 = A[T0 * 192 + 128 + lane];
   half8 y0, y1, y2;
@@ -550,8 +565,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const double* __restrict__ pinv64, const float* __restrict__ q32,
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
-                   int8_t* __restrict__ q_out, float* __restrict__ err_out, int nsplit,
-                   int split0, unsigned long long* __restrict__ split_keys) {
+                   int8_t* __restrict__ q_out, float* __restrict__ err_out, int nchunks,
+                   int chunk, int nconc_arg, unsigned long long* __restrict__ split_keys) {
   // With the record stage (kRec, P = 4 only) the per-wave pool holds the
   // candidate queue, the records (16 bounds and a meta word each) and the
   // per-slot threshold data; otherwise it is the queue alone.
@@ -582,6 +597,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   }
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
+  const int nconc = concurrent_ranges(nconc_arg, count, 4);
+  if (int(blockIdx.y) >= nconc) return;  // a range this rung does not need
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
 
   // ---------------------------------------------------------------- prologue
@@ -591,7 +608,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     const int64_t b = idx < count ? (list ? int64_t(list[begin + idx]) : idx) : 0;
     if (h == 0) {
       // a later launch of a sequential range split starts from the best so far
-      keys[nt * 32 + n] = split0 > 0 && idx < count ? split_keys[b] : ~0ull;
+      keys[nt * 32 + n] = chunk > 0 && idx < count ? split_keys[b] : ~0ull;
       blk[nt * 32 + n] = int32_t(b);
     }
     if constexpr (kRec) {
@@ -847,7 +864,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // errors start every block's best. (Longer pilots cost more matrix time than
   // the survivors they save.) Later launches of a sequential range split start
   // from the keys (setup() above has turned them into thresholds).
-  if (split0 == 0) {
+  if (chunk == 0) {
     const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
@@ -919,10 +936,10 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 
   // Seed-tile fragments; the index is clamped to the last tile so that every
   // load is unconditional and each wait covers only the tile it is for.
-  // Seed range split0 + blockIdx.y walks tiles [T0, T1) (at least 8 of them).
-  const int64_t rng = int64_t(split0) + blockIdx.y;
-  const int64_t T0 = rng * ntiles / nsplit;
-  const int64_t T1 = (rng + 1) * ntiles / nsplit;
+  // Range blockIdx.y of chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
+  const int64_t C0 = int64_t(chunk) * ntiles / nchunks, C1 = int64_t(chunk + 1) * ntiles / nchunks;
+  const int64_t T0 = C0 + int64_t(blockIdx.y) * (C1 - C0) / nconc;
+  const int64_t T1 = C0 + int64_t(blockIdx.y + 1) * (C1 - C0) / nconc;
   const int64_t last = T1 - 1;
   auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
     const half8* At = A + (T < last ? T : last) * 192;
@@ -1044,18 +1061,20 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 }
 
 // ---------------------------------------------------------------- seed ranges
-// The seed tiles of a rung can be walked in nsplit ranges: in sequence, one
+// The seed tiles of a rung can be walked in several ranges: in sequence, one
 // launch per chunk of kChunkTiles tiles, so that every wave walks the same 6 MB
 // of projector fragments at about the same time and they stay in L2 (one walk
 // over a 101 MB stack at K = 20 missed L2 on most requests); and, for a
-// uniform-rung search too small to fill the GPU, several ranges at once (grid
-// dimension y). The per-block keys of all ranges meet in a global minimum held
+// search too small to fill the GPU, several ranges at once (grid dimension y;
+// a multi-rung call's launch trims them to its rung's block count on the
+// GPU). The per-block keys of all ranges meet in a global minimum held
 // in the caller's mantissa output (8 bytes per block, 8-byte aligned); a later
 // launch starts from it, so the thresholds carry over and only the first one
 // runs the pilot. Keys order candidates by (error to 2^-28, seed) and every
 // range evaluates whatever could still win within it, so the final minimum is
 // the key the unsplit search ends with. A last pass emits each block's code.
 constexpr int64_t kChunkTiles = 2048;
+constexpr int64_t kRungRanges = 4;   // most concurrent ranges of a multi-rung rung's launch
 
 __device__ __forceinline__ bool rung_block(const int32_t* list, const int32_t* off, int rung,
                                            int64_t nblocks, int64_t i, int64_t& b) {
@@ -1167,23 +1186,34 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.exp_out = d_exp;
   a.q_out = d_q;
   a.err_out = d_err;
-  // sequential chunks of the seed tiles (SEEDQ_SEED_CHUNK_TILES overrides the
-  // chunk length; 0 = one chunk), then concurrent ranges within each chunk for
-  // a uniform-rung search (its block count is known here)
-  const int64_t chunk = env_int("SEEDQ_SEED_CHUNK_TILES", kChunkTiles);
-  const int64_t nseq = chunk > 0 ? std::max<int64_t>(1, std::min<int64_t>(L.ntiles / 8, L.ntiles / chunk)) : 1;
-  const int nconc = d_list ? 1 : seed_splits(nblocks, L.ntiles / nseq, P >= 4 ? 4 : 3);
-  const int nsplit = int(nseq) * nconc;
+  // Sequential chunks of the seed tiles (SEEDQ_SEED_CHUNK_TILES overrides the
+  // chunk length; 0 = one chunk), then concurrent ranges within each chunk:
+  // for a uniform-rung search the number follows from its block count, known
+  // here; a rung of a multi-rung call learns its count on the GPU, so its
+  // chunked launches (K >= 17) get up to kRungRanges ranges that each launch
+  // trims to what the count needs (nconc_arg < 0).
+  const int64_t chunk_tiles = env_int("SEEDQ_SEED_CHUNK_TILES", kChunkTiles);
+  const int64_t nseq =
+      chunk_tiles > 0 ? std::max<int64_t>(1, std::min<int64_t>(L.ntiles / 8, L.ntiles / chunk_tiles)) : 1;
+  const int64_t per_chunk = L.ntiles / nseq;
+  const int occ = P >= 4 ? 4 : 3;
+  int nconc_arg = 1;
+  if (!d_list)
+    nconc_arg = seed_splits(nblocks, per_chunk, occ);
+  else if (env_int("SEEDQ_SEED_SPLITS", 0) >= 1)
+    nconc_arg = seed_splits(1, per_chunk, occ);   // the override, clamped
+  else if (nseq > 1)
+    nconc_arg = -int(std::min<int64_t>(kRungRanges, std::max<int64_t>(1, per_chunk / 8)));
+  const int grid_y = nconc_arg > 0 ? nconc_arg : -nconc_arg;
   unsigned long long* keys = nullptr;
   const unsigned nb256 = unsigned((nblocks + 255) / 256);
-  if (nsplit > 1) {
+  if (nseq > 1 || grid_y > 1) {
     keys = reinterpret_cast<unsigned long long*>(d_q);
     hipLaunchKernelGGL(split_init_kernel, dim3(nb256), dim3(256), 0, stream, keys, nblocks, a.list,
                        a.off, a.rung);
   }
-  const dim3 grid = dim3(unsigned(blocks), unsigned(nconc), 1u);
+  const dim3 grid = dim3(unsigned(blocks), unsigned(grid_y), 1u);
   for (int64_t c = 0; c < nseq; ++c) {
-    const int split0 = int(c) * nconc;
     if constexpr (P >= 4) {
       auto kern = search_mfma_remat_kernel<P, false>;
       if constexpr (P == kRecordP)
@@ -1191,16 +1221,16 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
       hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0,
                          stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
                          reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
-                         a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, nsplit,
-                         split0, keys);
+                         a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, int(nseq),
+                         int(c), nconc_arg, keys);
     } else {
       hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
                          a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
                          a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
-                         nsplit, split0, keys);
+                         int(nseq), int(c), nconc_arg, keys);
     }
   }
-  if (nsplit > 1)
+  if (keys)
     hipLaunchKernelGGL(split_emit_kernel<P>, dim3(nb256), dim3(256), 0, stream, a.W, nblocks,
                        a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.seed_out, a.exp_out, a.q_out,
                        a.err_out);

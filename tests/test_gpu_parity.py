@@ -252,6 +252,41 @@ def test_search_seed_splits_match_unsplit(sq, torch, K, P):
             assert torch.equal(a, c), (K, P, label)
 
 
+def test_search_ranges_multi_rung_match_single_walk(sq, torch):
+    # a multi-rung call whose K = 17 rung is walked in sequential chunks with
+    # concurrent ranges that each launch sizes from the rung's block count on
+    # the GPU: the codes must equal those of one walk per rung, bit for bit
+    import os
+    rungs = ((10, 2), (17, 3))
+    nrows, ncols = 4, 8 * 150
+    W = synthetic.weights(nrows, ncols, 0.02, key=123, outlier_frac=0.02)
+    nb = nrows * ncols // 8
+    rob = (synthetic.splitmix64(123, synthetic.STREAM_MISC, nb) % np.uint64(2)).astype(np.uint8)
+    bases = [sq.build_bases(K, P) for K, P in rungs]
+    d, r = _dev(torch, W), _dev(torch, rob)
+    names = ("SEEDQ_SEED_CHUNK_TILES", "SEEDQ_SEED_SPLITS")
+    saved = {n: os.environ.get(n) for n in names}
+    out = {}
+    try:
+        for label, vals in {"single walk": ("0", "1"), "default": (None, None),
+                            "chunks of 128, 5 at once": ("128", "5")}.items():
+            for n, v in zip(names, vals):
+                if v is None:
+                    os.environ.pop(n, None)
+                else:
+                    os.environ[n] = v
+            out[label] = [t.cpu() for t in sq.compress(d, bases, rung_of_block=r)]
+    finally:
+        for n, v in saved.items():
+            if v is None:
+                os.environ.pop(n, None)
+            else:
+                os.environ[n] = v
+    for label in out:
+        for a, c in zip(out["single walk"], out[label]):
+            assert torch.equal(a, c), label
+
+
 def test_search_deterministic(sq, torch):
     W = synthetic.weights(32, 256, 0.02, key=8, outlier_frac=0.001)
     b = sq.build_bases(12, 3)
