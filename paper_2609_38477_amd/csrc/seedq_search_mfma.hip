@@ -1190,8 +1190,8 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   // chunk length; 0 = one chunk), then concurrent ranges within each chunk:
   // for a uniform-rung search the number follows from its block count, known
   // here; a rung of a multi-rung call learns its count on the GPU, so its
-  // chunked launches (K >= 17) get up to kRungRanges ranges that each launch
-  // trims to what the count needs (nconc_arg < 0).
+  // launches get up to kRungRanges ranges that each launch trims to what the
+  // count needs (nconc_arg < 0).
   const int64_t chunk_tiles = env_int("SEEDQ_SEED_CHUNK_TILES", kChunkTiles);
   const int64_t nseq =
       chunk_tiles > 0 ? std::max<int64_t>(1, std::min<int64_t>(L.ntiles / 8, L.ntiles / chunk_tiles)) : 1;
@@ -1202,8 +1202,8 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
     nconc_arg = seed_splits(nblocks, per_chunk, occ);
   else if (env_int("SEEDQ_SEED_SPLITS", 0) >= 1)
     nconc_arg = seed_splits(1, per_chunk, occ);   // the override, clamped
-  else if (nseq > 1)
-    nconc_arg = -int(std::min<int64_t>(kRungRanges, std::max<int64_t>(1, per_chunk / 8)));
+  else if (per_chunk >= 16)
+    nconc_arg = -int(std::min<int64_t>(kRungRanges, per_chunk / 8));
   const int grid_y = nconc_arg > 0 ? nconc_arg : -nconc_arg;
   unsigned long long* keys = nullptr;
   const unsigned nb256 = unsigned((nblocks + 255) / 256);
