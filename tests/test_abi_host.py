@@ -209,3 +209,15 @@ def test_empty_and_negative_shapes_are_argument_errors(sq, nrows, ncols):
         sq.plan_schedule(max(nrows, 0), max(ncols, 0), ((16, 3),), None, 4.0,
                          np.ones(max(ncols, 0), dtype=np.float32))
     assert e.value.code in (-1, -3)
+
+
+def test_plan_schedule_collinear_middle_rung_matches_oracle(oq):
+    # a middle rung on the chord of its neighbours is no hull vertex: the
+    # planner (host C++) and the oracle both drop it and allocate alike
+    import paper_2609_38477_amd as sq
+    rungs, damage = ((12, 2), (14, 2), (16, 2)), (4.0, 2.5, 1.0)
+    a = synthetic.importance_profile(64)
+    rob, rep = sq.plan_schedule(8, 64, rungs, damage, 3.25, a)
+    ref = oq.schedule(8, 64, rungs, damage, 3.25, a)
+    assert ref.hull == [0, 2] and list(rep["on_hull"]) == [1, 0, 1] and rep["nhull"] == 2
+    assert np.array_equal(rob, ref.rung_of_block)

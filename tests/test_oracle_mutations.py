@@ -1,12 +1,15 @@
 """The oracle's pins must catch plausible mistakes in the oracle itself.
 
-Each case plants one mistake in a copy of the oracle's C source (the copy
-only, never the file), compiles it on the CPU, and runs the oracle's pin
-tests against it in a subprocess (SEEDQ_ORACLE_LIB points the loader at the
-copy); at least one pin must fail. A control run of the unmodified copy must
-pass, so that a failure is the planted mistake's and not the harness's.
+Each case plants one mistake in a copy of the oracle (the copy only, never
+the files) and runs the oracle's pin tests against it in a subprocess; at
+least one pin must fail. The C half is compiled on the CPU from a mutated
+copy of its source (SEEDQ_ORACLE_LIB points the loader at it); the Python
+schedule runs from a copied package with a mutated allocation module. A
+control run of each unmodified copy must pass, so that a failure is the
+planted mistake's and not the harness's.
 """
 import os
+import shutil
 import subprocess
 import sys
 
@@ -66,4 +69,45 @@ def test_pins_catch_planted_mistake(tmp_path, name, old, new):
     assert old in text, f"{name}: the text to mutate is not in the oracle"
     lib = _build(tmp_path, text.replace(old, new))
     r = _run_pins(lib)
+    assert r.returncode == 1, f"{name}: no pin failed\n" + r.stdout[-2000:] + r.stderr[-2000:]
+
+
+# ---------------------------------------------------------------- schedule
+ALLOC = os.path.join(ROOT, "oracle", "allocation.py")
+SCHEDULE_MUTATIONS = [
+    ("floor as a ceiling", "imp = np.maximum(imp, q)", "imp = np.minimum(imp, q)"),
+    ("ties demoted from the end", "tied = np.nonzero(j_lo != j_hi)[0]         # ascending block index",
+     "tied = np.nonzero(j_lo != j_hi)[0][::-1]"),
+    ("rate without the exponent bits", "return K + 4 * P + 4", "return K + 4 * P"),
+    ("collinear hull points kept", "if cross <= 0:", "if cross < 0:"),
+]
+
+
+def _run_schedule_pins(tmp_path, alloc_text):
+    # a copy of the package layout the schedule pins import from
+    shutil.copytree(os.path.join(ROOT, "oracle"), tmp_path / "oracle",
+                    ignore=shutil.ignore_patterns("*.so", "__pycache__"))
+    (tmp_path / "oracle" / "allocation.py").write_text(alloc_text)
+    shutil.copy(os.path.join(ROOT, "synthetic.py"), tmp_path / "synthetic.py")
+    (tmp_path / "tests").mkdir()
+    for name in ("conftest.py", "test_oracle_schedule.py"):
+        shutil.copy(os.path.join(ROOT, "tests", name), tmp_path / "tests" / name)
+    env = dict(os.environ, SEEDQ_ORACLE_LIB=os.path.join(ROOT, "oracle", "liboq.so"))
+    return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                           "-m", "not gpu", "tests/test_oracle_schedule.py"], cwd=tmp_path,
+                          env=env, capture_output=True, text=True, timeout=600)
+
+
+def test_schedule_pins_pass_on_an_unmodified_copy(tmp_path, oq):
+    with open(ALLOC) as f:
+        r = _run_schedule_pins(tmp_path, f.read())
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
+
+
+@pytest.mark.parametrize("name,old,new", SCHEDULE_MUTATIONS, ids=[m[0] for m in SCHEDULE_MUTATIONS])
+def test_schedule_pins_catch_planted_mistake(tmp_path, oq, name, old, new):
+    with open(ALLOC) as f:
+        text = f.read()
+    assert old in text, f"{name}: the text to mutate is not in the schedule oracle"
+    r = _run_schedule_pins(tmp_path, text.replace(old, new))
     assert r.returncode == 1, f"{name}: no pin failed\n" + r.stdout[-2000:] + r.stderr[-2000:]

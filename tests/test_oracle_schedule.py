@@ -92,6 +92,11 @@ def test_hull_drops_non_convex_rung(oq):
     assert H == [0, 2]
     H = sch.hull(rates, np.array([4.0, 1.5, 1.0]))
     assert H == [0, 1, 2]
+    # a middle rung on the chord is no vertex of the hull (section 3.4: the
+    # ladder runs over the hull's vertices; a collinear rung buys no better
+    # damage per bit than mixing its neighbours)
+    H = sch.hull(rates, np.array([4.0, 2.5, 1.0]))
+    assert H == [0, 2]
 
 
 def test_decoder_reproduces_allocation(oq):
