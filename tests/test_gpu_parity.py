@@ -346,6 +346,56 @@ def test_search_full_size_attention_sampled(sq, oq, torch):
     check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx], "attn4096")
 
 
+# ---------------------------------------------------------------- widest register
+
+def _oracle_best_of(oq, w, K, P, seeds):
+    """Smallest exact quantised error over ``seeds`` (oracle, per seed)."""
+    U = np.stack([oq.basis(K, P, int(s)) for s in seeds])
+    t = oq.pinv_of(U) @ w.astype(np.float64)
+    es, qs = oq.quantize_numpy(t)
+    return min(oq.code_error(w, K, P, int(s), int(ee), qq) for s, ee, qq in zip(seeds, es, qs))
+
+
+@pytest.mark.parametrize("P", [1, 3, 4, 5, 6])
+def test_search_widest_register_k24(sq, oq, torch, P):
+    # K = 24: 2^24 - 1 seeds in 256 sequential chunks, seeds filling the 24 bits
+    # the keys and queue entries leave them, integer states at the 24-bit
+    # multiply's limit; every search variant (register walk at P = 1, 3; the
+    # rebuilding kernel with records at 4, lane masks at 5, the residual filter
+    # at 6). Planted codes come back exactly. At P = 1 the whole search is the
+    # oracle's; at larger P (the oracle's stack is too slow there) every random
+    # block's code is the oracle's quantised least-squares code of its seed, its
+    # error is exact, and no seed of a 16384-seed sample does better.
+    K = 24
+    nrand, nplant = (16, 8) if P == 1 else (8, 8)
+    Wr = synthetic.weights(1, 8 * nrand, 0.02, key=240 + P, outlier_frac=0.05).reshape(-1, 8)
+    ps, pe, pq = synthetic.random_codes(nplant, K, P, key=250 + P)
+    planted, _ = oq.decompress(ps, pe, pq, K, P)
+    blocks = np.concatenate([Wr, planted.reshape(-1, 8)]).astype(np.float32)
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(_dev(torch, blocks.reshape(1, -1)), [b])
+    torch.cuda.synchronize()
+    seed, e, q, err = seed.cpu().numpy().view(np.uint32), e.cpu().numpy(), q.cpu().numpy(), err.cpu().numpy()
+    assert not q[:, P:].any()
+    pl = slice(nrand, nrand + nplant)
+    assert np.array_equal(seed[pl], ps) and np.array_equal(e[pl], pe)
+    assert np.array_equal(q[pl, :P], pq)
+    if P == 1:
+        check_search(oq, blocks, K, P, seed, e, q, err, "k24")
+        return
+    sample = (synthetic.splitmix64(260 + P, synthetic.STREAM_MISC, 16384) % np.uint64((1 << K) - 1)
+              + np.uint64(1)).astype(np.int64)
+    for i in range(nrand):
+        w = blocks[i]
+        s = int(seed[i])
+        assert 1 <= s < (1 << K)
+        e_ref, q_ref = oq.quantize(oq.ls_solve(oq.basis(K, P, s), w.astype(np.float64)))
+        assert int(e[i]) == e_ref and np.array_equal(q[i, :P].astype(np.int64), q_ref), i
+        mine = oq.code_error(w, K, P, s, int(e[i]), q[i])
+        assert abs(float(err[i]) - mine) <= 1e-6 * mine + 1e-30, i
+        assert mine <= _oracle_best_of(oq, w, K, P, sample) * (1 + 2.0 ** -26), i
+
+
 # ---------------------------------------------------------------- decompress
 
 def test_decompress_bit_exact_multi_rung(sq, oq, torch):
