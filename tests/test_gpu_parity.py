@@ -396,6 +396,67 @@ def test_search_widest_register_k24(sq, oq, torch, P):
         assert mine <= _oracle_best_of(oq, w, K, P, sample) * (1 + 2.0 ** -26), i
 
 
+# ---------------------------------------------------------------- largest matrix
+
+def test_search_largest_block_count(sq, oq, torch):
+    # 32768 x 524280: 2^31 - 32768 blocks, the most a call accepts (69 GB of
+    # weights, drawn on the GPU from a seeded generator), so that every block
+    # index near 2^31 is exercised: a uniform search with planted codes at the
+    # start, the middle and the end, decompression of every block, then a
+    # two-rung search through the compaction lists; the oracle checks a sample
+    nrows, ncols = 32768, 524280
+    nb = nrows * (ncols // 8)
+    assert nb == (1 << 31) - 32768
+    g = torch.Generator(device="cuda").manual_seed(31)
+    W = torch.randn(nrows, ncols, device="cuda", generator=g).mul_(0.02)
+    K, P = 8, 1
+    at = np.concatenate([np.arange(16), (1 << 30) + np.arange(16), nb - 32 + np.arange(32)])
+    ps, pe, pq = synthetic.random_codes(len(at), K, P, key=311)
+    planted, _ = oq.decompress(ps, pe, pq, K, P)
+    Wb = W.view(-1, 8)
+    Wb[torch.from_numpy(at).cuda()] = torch.from_numpy(planted.reshape(-1, 8)).cuda()
+    sample = np.unique(np.concatenate([at, np.linspace(0, nb - 1, 384).astype(np.int64)]))
+    idx = torch.from_numpy(sample).cuda()
+    blocks = Wb[idx].cpu().numpy()
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(W, [b])
+    W_hat, _ = sq.decompress(seed, e, q, [(K, P)], nrows, ncols)
+    # every block: the reported error is that of its decompressed weights
+    worst = 0.0
+    for c0 in range(0, nb, 1 << 27):
+        c1 = min(nb, c0 + (1 << 27))
+        d = (Wb[c0:c1].double() - W_hat.view(-1, 8)[c0:c1].double()).pow_(2).sum(dim=1)
+        rel = (d - err[c0:c1].double()).abs_() / (d + 1e-30)
+        worst = max(worst, float(rel.max()))
+        del d, rel
+    assert worst <= 1e-5
+    s_, e_, q_, r_ = (seed[idx].cpu().numpy().view(np.uint32), e[idx].cpu().numpy(),
+                      q[idx].cpu().numpy(), err[idx].cpu().numpy())
+    pos = np.searchsorted(sample, at)
+    assert np.array_equal(s_[pos], ps) and np.array_equal(e_[pos], pe) and np.array_equal(q_[pos, :P], pq)
+    check_search(oq, blocks, K, P, s_, e_, q_, r_, "largest")
+    ref_w, _ = oq.decompress(s_, e_, q_, K, P)
+    assert np.array_equal(W_hat.view(-1, 8)[idx].cpu().numpy(), ref_w)
+    del seed, e, q, err, W_hat
+    torch.cuda.empty_cache()
+    # two rungs at random through the compaction lists
+    rungs = ((8, 1), (9, 2))
+    rob = torch.randint(0, 2, (nb,), dtype=torch.uint8, device="cuda", generator=g)
+    bases = [b, sq.build_bases(9, 2)]
+    seed, e, q, err = sq.compress(W, bases, rung_of_block=rob)
+    torch.cuda.synchronize()
+    r_of = rob[idx].cpu().numpy()
+    s_, e_, q_, r_ = (seed[idx].cpu().numpy().view(np.uint32), e[idx].cpu().numpy(),
+                      q[idx].cpu().numpy(), err[idx].cpu().numpy())
+    for r, (K, P) in enumerate(rungs):
+        sel = r_of == r
+        assert sel.sum() > 100
+        check_search(oq, blocks[sel], K, P, s_[sel], e_[sel], q_[sel], r_[sel], f"largest rung{r}")
+        assert not q_[sel][:, P:].any()
+    del W, Wb, seed, e, q, err, rob
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------- decompress
 
 def test_decompress_bit_exact_multi_rung(sq, oq, torch):
