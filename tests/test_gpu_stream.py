@@ -203,3 +203,78 @@ def test_gemv_stream_full_size(sq):
     Wn, xn = Wh.cpu().numpy(), x.cpu().numpy()
     ref = (Wn.astype(np.float64) @ xn.astype(np.float64).T).T
     assert np.all(np.abs(y - ref) <= _gemv_bound(Wn, xn).T)
+
+
+def test_stream_largest_block_count(sq, oq):
+    # 32768 x 524280 = 2^31 - 32768 blocks at two rungs (16 and 24 bits each, so
+    # about 4.3e10 stream bits, far past 2^32): random codes drawn on the GPU;
+    # pack then unpack returns every code, the one-pass decode equals the decode
+    # from code arrays bit for bit, a window of stream bits near the end equals
+    # the oracle packer's bits for the same blocks, and sampled rows of the
+    # decode-GEMV match the oracle's reconstruction times x in fp64
+    import torch
+    nrows, ncols = 32768, 524280
+    nb = nrows * (ncols // 8)
+    rungs = [(8, 1), (12, 2)]
+    g = torch.Generator(device="cuda").manual_seed(32)
+    rob = torch.randint(0, 2, (nb,), dtype=torch.uint8, device="cuda", generator=g)
+    seed = torch.randint(1, 1 << 8, (nb,), dtype=torch.int32, device="cuda", generator=g)
+    hi = torch.randint(1, 1 << 12, (nb,), dtype=torch.int32, device="cuda", generator=g)
+    sel = rob.bool()
+    seed = torch.where(sel, hi, seed)
+    del hi
+    exp = torch.randint(0, 16, (nb,), dtype=torch.uint8, device="cuda", generator=g)
+    q = torch.zeros((nb, 8), dtype=torch.int8, device="cuda")
+    q[:, 0] = torch.randint(-8, 8, (nb,), dtype=torch.int8, device="cuda", generator=g)
+    q[:, 1] = torch.randint(-8, 8, (nb,), dtype=torch.int8, device="cuda", generator=g) * sel
+    del sel
+    n1 = int(rob.sum(dtype=torch.int64))
+    cnt = [nb - n1, n1]
+    w = sq.pack(seed, exp, q, rungs, nrows, ncols, rob, cnt)
+    assert w.numel() * 32 >= 16 * (nb - n1) + 24 * n1 > (1 << 32)
+    s2, e2, q2 = sq.unpack(w, rungs, nrows, ncols, rob)
+    assert torch.equal(s2, seed) and torch.equal(e2, exp) and torch.equal(q2, q)
+    del s2, e2, q2
+    W1 = sq.decompress_stream(w, rungs, nrows, ncols, rob)
+    W2, _ = sq.decompress(seed, exp, q, rungs, nrows, ncols, rung_of_block=rob)
+    assert torch.equal(W1.view(torch.int32), W2.view(torch.int32))
+    del W2
+    # a window of 1000 blocks near the end against the oracle's packer
+    b0, b1 = nb - 1100, nb - 100
+    pre1 = int(rob[:b0].sum(dtype=torch.int64))
+    off = 16 * (b0 - pre1) + 24 * pre1
+    rw = rob[b0:b1].cpu().numpy()
+    ref = ostream.pack(seed[b0:b1].cpu().numpy().view(np.uint32), exp[b0:b1].cpu().numpy(),
+                       q[b0:b1].cpu().numpy(), rw, rungs)
+    L = int(16 * np.count_nonzero(rw == 0) + 24 * np.count_nonzero(rw == 1))
+    words = _words(w[off // 32: (off + L) // 32 + 1])
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little")[off % 32: off % 32 + L]
+    ref_bits = np.unpackbits(ref.view(np.uint8), bitorder="little")[:L]
+    assert np.array_equal(bits, ref_bits)
+    # sampled blocks of the decode against the oracle's reconstruction
+    idx = torch.from_numpy(np.concatenate([np.linspace(0, nb - 1, 512).astype(np.int64),
+                                           np.arange(nb - 64, nb)])).cuda()
+    r_of = rob[idx].cpu().numpy()
+    Ks = np.array([rungs[r][0] for r in r_of])
+    Ps = np.array([rungs[r][1] for r in r_of])
+    ref_w, _ = oq.decompress(seed[idx].cpu().numpy().view(np.uint32), exp[idx].cpu().numpy(),
+                             q[idx].cpu().numpy(), Ks, Ps)
+    assert np.array_equal(W1.view(-1, 8)[idx].cpu().numpy().view(np.uint32), ref_w.view(np.uint32))
+    del W1
+    torch.cuda.empty_cache()
+    # decode-GEMV, three sampled rows against the oracle in fp64
+    x = torch.randn(ncols, device="cuda", generator=g)
+    y = sq.gemv_stream(w, rungs, nrows, ncols, x, rob).cpu().numpy()
+    xn = x.cpu().numpy()
+    G = ncols // 8
+    for r in (0, nrows // 2, nrows - 1):
+        sl = slice(r * G, (r + 1) * G)
+        rr = rob[sl].cpu().numpy()
+        Wr, _ = oq.decompress(seed[sl].cpu().numpy().view(np.uint32), exp[sl].cpu().numpy(),
+                              q[sl].cpu().numpy(), np.array([rungs[k][0] for k in rr]),
+                              np.array([rungs[k][1] for k in rr]))
+        Wr = np.asarray(Wr, dtype=np.float32).reshape(1, ncols)
+        ref_y = float((Wr.astype(np.float64) @ xn.astype(np.float64))[0])
+        assert abs(float(y[r]) - ref_y) <= float(_gemv_bound(Wr, xn[None, :])[0, 0]), r
+    del w, seed, exp, q, rob, x
+    torch.cuda.empty_cache()
