@@ -212,6 +212,8 @@ def decoder_bench(args) -> int:
         hbm[f"dense_fp32_x{nv}"] = 4 * wl.nrows * wl.ncols + 4 * nv * (wl.ncols + wl.nrows)
     kernels = {k: {"ms": v, "hbm_bytes": hbm[k], "GBps": hbm[k] / (v / 1e3) / 1e9,
                    "hbm_frac": hbm[k] / (v / 1e3) / 1e9 / PEAK_HBM_GBS} for k, v in ms.items()}
+    if not args.no_cpu_baseline:
+        out_cpu = decoder_cpu_baseline(seed, exp, q, rob, rungs, args.cpu_seconds)
     out = {"metric": "decoder path: decoded weights/s and HBM GB/s per kernel; 1 GPU",
            "workload": wl.name, "shape": [wl.nrows, wl.ncols], "nblocks": nb,
            "rungs": [list(r) for r in rungs], "target_bpw": wl.target_bpw,
@@ -220,6 +222,137 @@ def decoder_bench(args) -> int:
            "decoded_weights_per_s": {k: 8 * nb / (v / 1e3) for k, v in ms.items()
                                      if k.startswith(("decompress", "gemv"))},
            "data": "synthetic"}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = out_cpu
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def decoder_cpu_baseline(seed, exp, q, rob, rungs, target_s: float) -> dict:
+    """The oracle's decoder on the GPU machine's host: the exact reconstruction
+    (C, one thread) on an evenly spaced sample of the searched codes, and the
+    bit-by-bit stream parser (Python) on a short run of them."""
+    import oracle
+    from oracle import stream as ostream
+    s_ = seed.cpu().numpy().view(np.uint32)
+    e_ = exp.cpu().numpy()
+    q_ = q.cpu().numpy()
+    r_ = np.asarray(rob, dtype=np.uint8)
+    Ks = np.array([k for k, _ in rungs], dtype=np.int64)[r_]
+    Ps = np.array([p for _, p in rungs], dtype=np.int64)[r_]
+    n = len(s_)
+    cal = np.arange(0, n, max(1, n // 4096))[:4096]
+    t0 = time.perf_counter()
+    oracle.decompress(s_[cal], e_[cal], q_[cal], Ks[cal], Ps[cal])
+    rate = len(cal) / (time.perf_counter() - t0)
+    m = int(min(n, max(4096, 0.6 * target_s * rate)))
+    idx = np.linspace(0, n - 1, m).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.decompress(s_[idx], e_[idx], q_[idx], Ks[idx], Ps[idx])
+    dt = time.perf_counter() - t0
+    nb_s = 2000
+    words = ostream.pack(s_[:nb_s], e_[:nb_s], q_[:nb_s], r_[:nb_s], rungs)
+    t0 = time.perf_counter()
+    ostream.unpack(words, r_[:nb_s], rungs)
+    dt_s = time.perf_counter() - t0
+    return {"value": 8 * m / dt, "unit": "decoded weights/s", "cores": 1, "kind": "oracle",
+            "stream_parse_blocks_per_s": nb_s / dt_s,
+            "sample": f"exact reconstruction of {m} evenly spaced blocks of the searched codes "
+                      f"in {dt:.1f} s (C, one thread); the bit-by-bit stream parser on the first "
+                      f"{nb_s} blocks in {dt_s:.2f} s"}
+
+
+def grid_bench(args) -> int:
+    """The rung grid (every rung S in 8..16, k in 2..6) on one matrix, one
+    uniform search per rung, and the oracle's exhaustive search timed on the host
+    over a sample of the same blocks at every rung."""
+    import torch
+
+    import synthetic
+    from paper_2609_38477_amd import grid
+
+    wl = synthetic.WORKLOADS[args.workload]
+    W = synthetic.workload_weights(wl)
+    dW = torch.from_numpy(W).cuda()
+    grid.build_grid(dW, rungs=((8, 2),))    # warm-up
+    res = grid.build_grid(dW, rungs=grid.PAPER_GRID)
+    total_c = sum(res.candidates(r) for r in res.rungs)
+    total_ms = sum(res.search_ms.values())
+    out = {"metric": "rung grid: block·seed candidates/s over 45 uniform searches; 1 GPU",
+           "value": total_c / (total_ms / 1e3), "unit": "block·seed candidates/s",
+           "workload": wl.name, "shape": [wl.nrows, wl.ncols], "nblocks": res.nblocks,
+           "rungs": len(res.rungs), "search_ms_total": total_ms, "candidates_total": total_c,
+           "per_rung_ms": {f"{r[0]},{r[1]}": res.search_ms[r] for r in res.rungs},
+           "data": "synthetic"}
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+        blocks = W.reshape(-1, 8)
+        nbs = 256
+        sample = np.ascontiguousarray(blocks[np.linspace(0, len(blocks) - 1, nbs).astype(np.int64)])
+        dt, cands = 0.0, 0
+        for K, P in res.rungs:
+            pinv = oracle.cached_pinv_stack(K, P)
+            t0 = time.perf_counter()
+            oracle.search(sample, K, P, threads=threads, pinv=pinv)
+            dt += time.perf_counter() - t0
+            cands += nbs * ((1 << K) - 1)
+            oracle._PINV_CACHE.clear()
+        out["cpu_baseline"] = {"value": cands / dt, "unit": "block·seed candidates/s",
+                               "cores": int(threads), "kind": "oracle",
+                               "sample": f"{nbs} evenly spaced blocks of the same matrix at each of "
+                                         f"the {len(res.rungs)} rungs, {cands:.3g} candidates in "
+                                         f"{dt:.1f} s; pseudo-inverses precomputed outside the "
+                                         f"timed region"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def frontend_bench(args) -> int:
+    """The data-free importance of one 7B-shaped synthetic layer (a of all
+    seven projections, rho, channel orders, column statistics and outlier
+    columns) on the GPU, and the oracle's fp64 numpy version of the same on the
+    host."""
+    import torch
+
+    import synthetic
+    from paper_2609_38477_amd import frontend
+
+    L = synthetic.synthetic_layer(4096, 11008, 32, 8, 32000)
+    dW = {n: torch.from_numpy(np.ascontiguousarray(L.tensors[n])).cuda()
+          for n in (*frontend.PROJECTIONS, "lm_head")}
+    frontend.layer_importance(L, dW)     # warm-up
+    torch.cuda.synchronize()
+    reps = 3
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        imp = frontend.layer_importance(L, dW)
+    torch.cuda.synchronize()
+    gpu_s = (time.perf_counter() - t0) / reps
+    out = {"metric": "importance front end: seconds per 7B-shaped layer; 1 GPU",
+           "value": gpu_s, "unit": "s", "higher_is_better": False,
+           "layer": {"d": 4096, "f": 11008, "heads": 32, "kv_heads": 8, "vocab": 32000},
+           "outliers": [list(o) for o in imp.outliers], "data": "synthetic"}
+    if not args.no_cpu_baseline:
+        from oracle import importance as oimp
+        T = L.tensors
+        t0 = time.perf_counter()
+        a_attn = oimp.gamma_importance(L.gains["attn"])
+        a_mlp = oimp.gamma_importance(L.gains["mlp"])
+        ref = {"q": a_attn, "k": a_attn, "v": a_attn, "gate": a_mlp, "up": a_mlp,
+               "o": oimp.propagate_o(T["v"], a_attn.astype(np.float32), L.n_heads, L.n_kv_heads),
+               "down": oimp.propagate_down(T["gate"], T["up"], a_mlp.astype(np.float32))}
+        oimp.rho_from_head(T["lm_head"])
+        for n in frontend.PROJECTIONS:
+            oimp.channel_order(ref[n].astype(np.float32))
+        names = list(frontend.PROJECTIONS)
+        want = oimp.outlier_columns([T[n] for n in names], [ref[n] for n in names])
+        cpu_s = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": cpu_s, "unit": "s", "cores": 1, "kind": "oracle",
+                               "same_outliers": [(names[t], c) for t, c in want] ==
+                                                [tuple(o) for o in imp.outliers],
+                               "sample": "the whole layer (the oracle's numpy fp64 path; BLAS "
+                                         "threads as numpy configures them)"}
     print(json.dumps(out), flush=True)
     return 0
 
@@ -233,6 +366,10 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-gemm-reference", action="store_true")
+    ap.add_argument("--grid", action="store_true",
+                    help="time the 45-rung grid (S in 8..16, k in 2..6) with the oracle beside it")
+    ap.add_argument("--frontend", action="store_true",
+                    help="time the importance front end on a 7B-shaped layer with the oracle beside it")
     ap.add_argument("--decoder", action="store_true",
                     help="time the decoder path (derive, pack, parse, decode, decode-GEMV) instead")
     ap.add_argument("--gemm-reference-only", action="store_true",
@@ -258,6 +395,10 @@ def main() -> int:
         return 2
     if args.decoder:
         return decoder_bench(args)
+    if args.grid:
+        return grid_bench(args)
+    if args.frontend:
+        return frontend_bench(args)
     wl = synthetic.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
