@@ -229,7 +229,7 @@ def decoder_bench(args) -> int:
 
 
 def decoder_cpu_baseline(seed, exp, q, rob, rungs, target_s: float) -> dict:
-    """The oracle's decoder on the GPU machine's host: the exact reconstruction
+    """The oracle's decoder on the host: the exact reconstruction
     (C, one thread) on an evenly spaced sample of the searched codes, and the
     bit-by-bit stream parser (Python) on a short run of them."""
     import oracle
