@@ -1,4 +1,5 @@
 // C ABI entry points of libseedq.so: argument checks and launches.
+#include <cmath>
 #include <cstring>
 
 #include "seedq_internal.h"
@@ -307,6 +308,8 @@ int seedq_expect_silu_sq(const double* d_var, int64_t n, int32_t nodes, double* 
 
 int seedq_channel_order(const float* a, int64_t n, int32_t* perm) {
   if (!a || !perm || n < 0 || n > (int64_t(1) << 31) - 1) return SEEDQ_EINVAL;
+  for (int64_t i = 0; i < n; ++i)
+    if (!std::isfinite(a[i])) return SEEDQ_EINVAL;   // the sort needs a total order
   channel_order(a, n, perm);
   return SEEDQ_OK;
 }

@@ -58,3 +58,12 @@ def test_select_outliers_matches_oracle(sq):
     a = np.ones(100)
     assert sq.seedq_select_outliers([st[0]], [st[1]], [a], keep=4) == oimp.outlier_columns([W], [a])
     assert sq.seedq_select_outliers([st[0]], [st[1]], [a], keep=0) == []
+
+
+def test_channel_order_rejects_non_finite_importance():
+    import paper_2609_38477_amd as sq
+    for bad in (np.nan, np.inf, -np.inf):
+        a = np.array([1.0, bad, 0.5], dtype=np.float32)
+        with pytest.raises(sq.SeedqError) as e:
+            sq.seedq_channel_order(a)
+        assert e.value.code == -1
