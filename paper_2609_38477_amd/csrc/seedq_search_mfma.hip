@@ -477,8 +477,13 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     const uint32_t t32 = uint32_t(T);
 #pragma unroll
     for (int pr = 0; pr < 2; ++pr) {
+      // raised issue priority while this wave feeds the matrix core, so that
+      // its products start ahead of the other waves' folds (measured +0.5 to
+      // +1.1 % at (16,3); the rebuilding kernel measured slower with it)
+      __builtin_amdgcn_s_setprio(1);
       const floatx16 acc0 = bounds(a0, a1, a2, bop[2 * pr]);
       const floatx16 acc1 = bounds(a0, a1, a2, bop[2 * pr + 1]);
+      __builtin_amdgcn_s_setprio(0);
       const bool p0 = fold_max(acc0) >= thr[2 * pr];
       const bool p1 = fold_max(acc1) >= thr[2 * pr + 1];
       const uint64_t m0 = ballot(p0), m1 = ballot(p1);
