@@ -204,6 +204,30 @@ def test_search_every_kernel_variant_in_one_call(sq, oq, torch):
         assert not q[sel][:, P:].any()
 
 
+def test_search_without_error_output_gives_the_same_codes(sq, torch):
+    # d_err is optional: with it NULL every kernel variant (register walk,
+    # rebuilding kernel with and without records, lane masks, residual filter,
+    # sequential chunks and the emission pass of split walks) must give the
+    # same codes bit for bit
+    cases = [(((10, 2), (13, 4), (11, 5), (15, 6), (17, 3)), 4, 8 * 61),
+             (((18, 4),), 2, 8 * 40),
+             (((12, 3),), 3, 8 * 97)]
+    for rungs, nrows, ncols in cases:
+        W = synthetic.weights(nrows, ncols, 0.02, key=500 + len(rungs) + ncols, outlier_frac=0.02)
+        nb = nrows * ncols // 8
+        rob = None
+        if len(rungs) > 1:
+            rob = _dev(torch, (synthetic.splitmix64(501, synthetic.STREAM_MISC, nb)
+                               % np.uint64(len(rungs))).astype(np.uint8))
+        bases = [sq.build_bases(K, P) for K, P in rungs]
+        a = sq.compress(_dev(torch, W), bases, rung_of_block=rob)
+        b = sq.compress(_dev(torch, W), bases, rung_of_block=rob, with_err=False)
+        torch.cuda.synchronize()
+        assert b[3] is None
+        for x, y in zip(a[:3], b[:3]):
+            assert torch.equal(x, y), rungs
+
+
 def test_invalid_rung_index_gets_seed_zero(sq, torch):
     rungs = ((8, 2), (10, 3))
     W = synthetic.weights(2, 64, 0.02, key=3)
