@@ -297,7 +297,7 @@ def grid_bench(args) -> int:
             oracle.search(sample, K, P, threads=threads, pinv=pinv)
             dt += time.perf_counter() - t0
             cands += nbs * ((1 << K) - 1)
-            oracle._PINV_CACHE.clear()
+            oracle.clear_pinv_cache()
         out["cpu_baseline"] = {"value": cands / dt, "unit": "block·seed candidates/s",
                                "cores": int(threads), "kind": "oracle",
                                "sample": f"{nbs} evenly spaced blocks of the same matrix at each of "
