@@ -39,12 +39,19 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-# The search kernel's dense contraction: for every (block, seed) candidate the
-# least-squares bound w^T Pi_s w over the 36 pair products of the block, i.e.
-# 36 multiply-adds = 72 flops on fp16 matrix cores (the kernel issues the 36
-# padded to 48).
-SEARCH_FLOPS_PER_CANDIDATE = 72.0
-SEARCH_ISSUED_FLOPS_PER_CANDIDATE = 96.0
+# Roofline work of the search (the least-squares projection of every block on
+# every seed's basis): 2 C P flops per (block, seed) candidate, i.e. 48 at
+# P = 3, priced against the dense fp16 matrix-core peak because the contraction
+# the kernel issues is fp16. Two other counts are reported beside it under
+# their own keys: the kernel's quadratic form over the 36 pair products of a
+# block (72 flops per candidate at every P) and what it issues (the 36 pairs
+# padded to 48 reduction slots: 96 flops per candidate).
+def projection_flops(K: int, P: int) -> float:
+    return float((1 << K) - 1) * 2 * 8 * P
+
+
+QUADFORM_FLOPS_PER_CANDIDATE = 72.0
+ISSUED_FLOPS_PER_CANDIDATE = 96.0
 
 
 def kernel_source_hash() -> str:
@@ -366,6 +373,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-gemm-reference", action="store_true")
+    ap.add_argument("--no-target-layer", action="store_true",
+                    help="leave out the 4096x14336 three-rung layer timed after the headline")
     ap.add_argument("--grid", action="store_true",
                     help="time the 45-rung grid (S in 8..16, k in 2..6) with the oracle beside it")
     ap.add_argument("--frontend", action="store_true",
@@ -399,9 +408,50 @@ def main() -> int:
         return grid_bench(args)
     if args.frontend:
         return frontend_bench(args)
+    torch.cuda.set_device(torch.device("cuda:0"))
     wl = synthetic.WORKLOADS[args.workload]
+    out, W = run_steps(wl, args.steps, args.warmup)
+    out = {"metric": METRIC, **out}
+    if args.workload == "attn4096" and not args.no_target_layer:
+        # the 4096 x 14336 layer with the three-rung schedule, timed the same way
+        tl = synthetic.WORKLOADS["mlp_up"]
+        log(f"target layer {tl.name}: {TARGET_LAYER_STEPS} timed steps")
+        t_out, _ = run_steps(tl, TARGET_LAYER_STEPS, 1)
+        out["target_layer"] = {k: t_out[k] for k in (
+            "value", "unit", "steps", "warmup", "ms_per_step", "config", "roofline",
+            "roofline_other_counts", "phases_ms", "search_candidates_per_s")}
+    if not args.no_gemm_reference:
+        log("timing a 16384^3 fp16 GEMM on random data as the practical matrix-core reference")
+        ref = practical_mfma_tflops()
+        search_s = out["phases_ms"]["search"] / 1000.0
+        cands = out["config"]["candidates_per_step"]
+        issued = cands * ISSUED_FLOPS_PER_CANDIDATE / search_s / 1e12
+        out["mfma_practical"] = {
+            "reference": "torch.matmul fp16 16384x16384x16384, N(0,1) operands (hipBLASLt)",
+            "reference_tflops": ref, "search_issued_tflops": issued,
+            "search_issued_over_reference": issued / ref,
+            "search_roofline_work_over_reference": out["roofline"]["achieved"] / ref}
+    if not args.no_cpu_baseline:
+        rungs = list(wl.rungs)
+        K, P = rungs[0] if len(rungs) == 1 else rungs[1]
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(W, K, P, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+TARGET_LAYER_STEPS = 3
+
+
+def run_steps(wl, steps: int, warmup: int):
+    """Whole-path steps on one workload: W untimed, then exactly `steps` timed
+    between synchronisations. Returns the result fields and the host matrix."""
+    import torch
+
+    import paper_2609_38477_amd as sq
+    import synthetic
+
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
     log(f"workload {wl.name}: {wl.note}")
     W = synthetic.workload_weights(wl)
@@ -427,7 +477,6 @@ def main() -> int:
         return {k: torch.cuda.Event(enable_timing=True) for k in ("start", "bases", "search", "decomp")}
 
     plan_s = []
-
     rep_counts = [0] * R
 
     def step(ev):
@@ -449,76 +498,71 @@ def main() -> int:
         ev["decomp"].record(stream)
         return cands
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(events())
         torch.cuda.synchronize()
-        log(f"warmup step {i + 1}/{args.warmup} done")
+        log(f"{wl.name}: warmup step {i + 1}/{warmup} done")
     # timed region: exactly `steps` steps, events recorded on the stream the
     # kernels run on, read after the closing synchronisation
-    evs = [events() for _ in range(args.steps)]
+    evs = [events() for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         cands = step(evs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    log(f"{args.steps} timed steps done in {t1 - t0:.3f} s")
+    log(f"{wl.name}: {steps} timed steps done in {t1 - t0:.3f} s")
     phase = {"bases": [e["start"].elapsed_time(e["bases"]) for e in evs],
              "search": [e["bases"].elapsed_time(e["search"]) for e in evs],
              "decomp": [e["search"].elapsed_time(e["decomp"]) for e in evs]}
-    ms = (t1 - t0) * 1000.0 / args.steps
+    ms = (t1 - t0) * 1000.0 / steps
     value = cands / (ms / 1000.0)
 
     search_ms = float(np.mean(phase["search"]))
     decomp_ms = float(np.mean(phase["decomp"]))
     bases_ms = float(np.mean(phase["bases"]))
-    # dominant kernel: the search (one launch per rung; one launch in total for
-    # a single-rung workload)
-    flops = float(cands) * SEARCH_FLOPS_PER_CANDIDATE
+    # dominant kernel: the search (one launch per rung, or per seed chunk of a
+    # K >= 17 rung), timed by the events around seedq_compress on its stream
+    flops = sum(rep_counts[r] * projection_flops(K, P) for r, (K, P) in enumerate(rungs))
     achieved = flops / (search_ms / 1000.0) / 1e12
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP16_MFMA_TFLOPS,
                 "unit": "TFLOP/s", "frac": achieved / PEAK_FP16_MFMA_TFLOPS,
-                "traffic": measured_traffic(wl.name)}
+                "traffic": measured_traffic(wl.name),
+                "work": "2*C*P flops per block-seed candidate (the least-squares projection)"}
+    other = {}
+    for key, per in (("quadratic_form", QUADFORM_FLOPS_PER_CANDIDATE),
+                     ("issued", ISSUED_FLOPS_PER_CANDIDATE)):
+        t = cands * per / (search_ms / 1000.0) / 1e12
+        other[key] = {"flops_per_candidate": per, "achieved": t,
+                      "frac": t / PEAK_FP16_MFMA_TFLOPS}
 
     # The direct design -- project every block onto every seed's pseudo-inverse
     # on fp32 matrix cores (2 C P flops per candidate), then quantise each
     # candidate -- is capped at 157.3e12 / (2 C P) candidates/s even before its
     # epilogue; the quadratic-form screen above replaces that projection.
-    flops_direct = float(sum(int(rep_counts[r]) * ((1 << K) - 1) * 2 * 8 * P
-                             for r, (K, P) in enumerate(rungs)))
-    direct_ceiling = cands / (flops_direct / (PEAK_FP32_MFMA_TFLOPS * 1e12))
+    direct_ceiling = cands / (flops / (PEAK_FP32_MFMA_TFLOPS * 1e12))
     out = {
-        "metric": METRIC, "value": value, "unit": "block·seed candidates/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "value": value, "unit": "block·seed candidates/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": ms, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
         "config": {"workload": wl.name, "shape": [wl.nrows, wl.ncols], "C": 8,
                    "rungs": [list(r) for r in rungs], "target_bpw": wl.target_bpw,
-                   "nblocks": nb, "candidates_per_step": cands, "description": wl.note},
+                   "nblocks": nb, "blocks_per_rung": list(rep_counts),
+                   "candidates_per_step": cands, "description": wl.note},
         "roofline": roofline,
-        "phases_ms": {"plan_host": 1000.0 * float(np.mean(plan_s[-args.steps:])), "bases": bases_ms,
+        "roofline_other_counts": other,
+        "phases_ms": {"plan_host": 1000.0 * float(np.mean(plan_s[-steps:])), "bases": bases_ms,
                       "search": search_ms, "decompress": decomp_ms},
         "search_candidates_per_s": cands / (search_ms / 1000.0),
         "fp32_projection_ceiling": {
-            "candidates_per_s": direct_ceiling, "flops_per_candidate": flops_direct / cands,
+            "candidates_per_s": direct_ceiling, "flops_per_candidate": flops / cands,
             "peak_tflops": PEAK_FP32_MFMA_TFLOPS,
             "search_over_ceiling": cands / (search_ms / 1000.0) / direct_ceiling},
         "decompress_GBps": nb * (14 + 32) / (decomp_ms / 1000.0) / 1e9,
     }
-    if not args.no_gemm_reference:
-        log("timing a 16384^3 fp16 GEMM on random data as the practical matrix-core reference")
-        ref = practical_mfma_tflops()
-        issued = float(cands) * SEARCH_ISSUED_FLOPS_PER_CANDIDATE / (search_ms / 1000.0) / 1e12
-        out["mfma_practical"] = {
-            "reference": "torch.matmul fp16 16384x16384x16384, N(0,1) operands (hipBLASLt)",
-            "reference_tflops": ref, "search_issued_tflops": issued,
-            "search_issued_over_reference": issued / ref,
-            "search_algorithmic_over_reference": achieved / ref}
-    if not args.no_cpu_baseline:
-        K, P = rungs[0] if R == 1 else rungs[1]
-        log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(W, K, P, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
-    return 0
+    del dW, bases, seed, exp, q, err, W_hat, ws, d_rob
+    torch.cuda.empty_cache()
+    return out, W
 
 
 if __name__ == "__main__":

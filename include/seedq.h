@@ -11,12 +11,12 @@
  * seed s, P signed 4-bit mantissas q and one shared 4-bit exponent e, so that
  *     w_hat = U(s) * q * 2^-e,                        (section 3.1, eq. (codec))
  * costing K + 4P + 4 bits                              (section 3.1, eq. (rate)).
- * U(s) (8 x P) is generated by a maximal-length K-bit LFSR started at state s
- * (section 3.1): Galois right-shift steps x <- (x >> 1) ^ (x & 1 ? mask_K : 0),
+ * U(s) (8 x P) comes from a full-period K-bit LFSR whose initial state is the
+ * seed s (section 3.1): Galois right-shift steps x <- (x >> 1) ^ (x & 1 ? mask_K : 0),
  * column j holds the states x_{8j} .. x_{8j+7} centred as x - 2^(K-1), and
  * U = U_int * 2^-(K-1), entries in [-1, 1).
- * The encoder searches all 2^K - 1 seeds for the smallest quantised error
- * (section 3.1): t* = pinv(U(s)) w is the minimum-norm least-squares fit
+ * The encoder tries every nonzero seed and keeps the code of least quantised
+ * error (section 3.1): t* = pinv(U(s)) w is the minimum-norm least-squares fit
  * (singular values at or below 2^-30 of the largest count as zero), e is the
  * largest exponent in [0, 15] at which every round-half-even mantissa
  * rne(t*_j 2^e) lies in [-8, 7] (e = 0, mantissas clamped, if none does), and the
@@ -175,9 +175,9 @@ typedef struct {
 size_t seedq_compress_workspace_bytes(int64_t nrows, int64_t ncols, int32_t C, int32_t nrungs);
 
 /*
- * The per-block exhaustive seed search (section 3.1; its cost, 2^K
- * least-squares fits per block, is the encoder's dominant cost per the appendix
- * on cost): for every block, the code (seed, e, q) of smallest exact quantised
+ * The per-block exhaustive seed search (section 3.1; the appendix on cost
+ * names it, one least-squares fit per block and seed, as what the encoder spends
+ * its time on): for every block, the code (seed, e, q) of smallest exact quantised
  * error over all 2^K - 1 seeds of the block's rung, ties to the smallest seed.
  *   d_W:             device fp32 [nrows][ncols], row-major, finite values,
  *                    32-byte aligned (one block per 32 bytes).
@@ -212,8 +212,8 @@ int seedq_compress(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
 
 /*
  * Reconstruction w_hat = U(s) q 2^-e for every block (Algorithm 2, the
- * reconstruction step; one LFSR expansion and P multiply-accumulates per weight,
- * per the appendix on cost). The integer reconstruction acc_i = sum_j
+ * reconstruction step; per the appendix on cost the decoder regenerates the
+ * LFSR states and does P multiply-adds for each weight). The integer reconstruction acc_i = sum_j
  * U_int[i][j] q_j is exact; w_hat_i = acc_i * 2^-(K-1+e) rounded once to fp32.
  *   d_seed, d_exp, d_q: codes as written by seedq_compress.
  *   d_rung_of_block:    device uint8 [nblocks] or NULL when nrungs == 1.
@@ -232,9 +232,10 @@ int seedq_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t*
 /*
  * The headerless variable-length code stream of one tensor (Algorithm 1, the
  * emit step: block b contributes exactly l(g_b) = K + 4P + 4 bits, eq. (rate),
- * with no header; Algorithm 2 and the appendix on encoding and decoding: blocks
- * are parsed left to right, their lengths known from the rung allocation alone,
- * so a fault in one block's bits changes that block only).
+ * with no header; Algorithm 2 and the appendix on encoding and decoding: a
+ * decoder reads the blocks in order from the start, the length of each known
+ * from the rung allocation alone, so a fault in one block's bits changes that
+ * block only).
  * Layout (the paper fixes none): blocks in row-major order; inside a block the
  * seed (K bits), the exponent e (4 bits), then q_0 .. q_{P-1} (4 bits each, two's
  * complement); every field least-significant bit first at increasing stream bit
@@ -304,8 +305,8 @@ int seedq_decompress_stream(const uint32_t* d_stream, size_t stream_bytes,
 /*
  * Decode-GEMV straight from the stream: y_v = W_hat x_v for nvec right-hand
  * sides, W_hat decoded on the fly and never stored (the codec's bandwidth
- * motivation, section 1 and the appendix on cost: one LFSR expansion and P
- * multiply-accumulates per weight at the decoder). Every weight is the one
+ * motivation, section 1; per the appendix on cost the decoder regenerates the
+ * LFSR states and does P multiply-adds for each weight). Every weight is the one
  * seedq_decompress_stream would write; the products are accumulated in fp32,
  * each lane over every 64th block of the row, then a tree across the lanes.
  *   nvec:  1, 2, 4 or 8.
@@ -397,8 +398,8 @@ int seedq_permute_columns(const float* d_in, int64_t nrows, int64_t ncols, const
 /* Outlier columns over a model (appendix on outlier columns): column j of tensor
  * t is a candidate when maxabs/(median + 2^-24 maxabs) >= 1e3 or a_j >= 1e2 times
  * the tensor's mean a; each rule keeps its 32 largest statistics (ties by
- * tensor, then column), candidates are ranked by their better position in the
- * two lists (ties by tensor, then column) and the first `keep` are written to
+ * tensor, then column), a candidate's rank is the smaller of its two list
+ * positions (ties by tensor, then column) and the first `keep` are written to
  * out_tensor / out_col (host arrays of at least keep), *out_count how many.
  * maxabs, median, a: host fp64 arrays [ntensors][ncols[t]] (e.g. from
  * seedq_column_stats and the propagation). Host only. Errors: SEEDQ_EINVAL. */
@@ -406,8 +407,8 @@ int seedq_select_outliers(int32_t ntensors, const int64_t* ncols, const double* 
                           const double* const* median, const double* const* a, int32_t keep,
                           int32_t* out_tensor, int32_t* out_col, int32_t* out_count);
 
-/* FP16 escape of whole columns (appendix on outlier columns: stored in FP16 and
- * overwriting the codec's reconstruction at the decoder). extract: d_fp16
+/* FP16 escape of whole columns (appendix on outlier columns: such columns are
+ * kept in FP16, and the decoder writes them over the decoded weights). extract: d_fp16
  * [ncol][nrows] (device fp16) = round-to-nearest-even of W[:, cols[i]];
  * apply: W[:, cols[i]] = d_fp16[i][:] widened to fp32. d_cols: device int32
  * [ncol]; an index outside [0, ncols) extracts NaN and applies nothing.

@@ -8,8 +8,8 @@ Everything here is the plain, slow definition of what the Seed-Q encoder
 computes for one weight matrix, in fp64:
 
 * ``states`` / ``basis_int``: the LFSR basis U(s) of section 3.1, eq. (codec)
-  ("generated by a maximal-length S-bit LFSR started at state s"; the hardware
-  appendix adds centred states and width-dependent taps). Reading: Galois
+  (a full-period S-bit LFSR whose initial state is the seed s; per the hardware
+  appendix its states are centred and its taps depend on the width). Reading: Galois
   right-shift LFSR with the mask table in ``seedq_oracle.c``, column j of U holds
   the centred states x_{8j}..x_{8j+7}, U = U_int * 2^-(K-1).
 * ``pinv_stack``: per-seed Moore-Penrose pseudo-inverse of U(s) (LAPACK SVD via
@@ -21,8 +21,8 @@ computes for one weight matrix, in fp64:
 * ``code_error``: ||w - U(s) q 2^-e||^2 with exact integer reconstruction.
 * ``search`` (C, OpenMP) and ``search_numpy`` (vectorised numpy): the
   exhaustive search of section 3.1 over all 2^K - 1 seeds, ties to the smallest
-  seed. The appendix on cost (section A.8) states that this search, 2^S
-  least-squares fits per block, dominates the encoder.
+  seed. Per the appendix on cost (section A.8) the encoder's time goes into
+  this search, one least-squares fit for every seed of every block.
 * ``decompress``: w_hat = U(s) t_hat (Algorithm 2), exact.
 * ``schedule``: the allocation of sections 3.2-3.4 (eq. (objective), (imp),
   the floor, eq. (ladder), Everett bisection and the tie pass of Algorithm 1).

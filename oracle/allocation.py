@@ -2,7 +2,7 @@
 
 Follows the paper's allocation in its own order (Algorithm 1, first five steps):
 
-1. lower convex hull of {(r(g), e(g))}, slopes s_j = (e_j - e_{j+1}) / (r_{j+1} - r_j)
+1. the rungs' (rate, damage) points {(r(g), e(g))} reduced to their lower convex hull, slopes s_j = (e_j - e_{j+1}) / (r_{j+1} - r_j)
    (section 3.4, "Damage curve and hull");
 2. block importance imp_b = abar_b * rho_{r(b)}, abar_b the mean of a_j over the
    block's 8 columns, both factors normalised to unit mean within the tensor
@@ -12,9 +12,9 @@ Follows the paper's allocation in its own order (Algorithm 1, first five steps):
 4. lambda by bisection so that the mean rate meets the target (eq. (lagrangian),
    Everett's theorem, appendix on ties), blocks ranked by the ladder
    j(b) = 1 + |{j : lambda / s_j <= imp_b}| (eq. (ladder));
-5. tie pass: the tied group at the final threshold is demoted in block order
-   until the budget is met (section 3.4, Algorithm 2 "the first T_t tied blocks
-   taking the lower rung").
+5. tie pass: blocks of the tied group at the final threshold are lowered one
+   rung, earliest first, until the total fits the budget (section 3.4;
+   Algorithm 2 lowers T_t of them).
 
 Readings where the paper is silent: the f-quantile is the inverted-CDF
 (lower) empirical quantile over blocks; block order is the row-major block

@@ -15,10 +15,10 @@ Plain fp64 numpy, in the paper's order:
   blocking (paragraph on block importance);
 * outlier columns (appendix on outlier columns): a column is a candidate when
   max_i |W_ij| / (median_i |W_ij| + eps) >= 1e3 or a_j >= 1e2 times the
-  tensor mean of a; each rule keeps at most its 32 largest values (ties by
-  tensor, then column index), each list is ordered by its own statistic, the
-  candidates are ranked by their better position in the two lists (ties by
-  tensor, then column) and the first four are kept.
+  tensor mean of a; a rule's list holds up to 32 candidates, those with the
+  largest statistic (ties by tensor, then column index), in decreasing order
+  of it; a candidate's rank is the smaller of its two list positions (ties by
+  tensor, then column) and the four best ranked are kept.
 
 Readings where the paper is silent: the quadrature uses 128 Gauss-Hermite
 nodes (relative error below 1e-12 for variances up to 4, 2.4e-6 at 25);
@@ -84,7 +84,8 @@ def propagate_down(W_gate, W_up, a_in, nodes: int = 128) -> np.ndarray:
 
 
 def rho_from_head(W_lm) -> np.ndarray:
-    """Residual-stream gradient scale from an isotropic gradient at the logits."""
+    """Row scale of the residual stream: a unit gradient at every logit carried
+    back through the output head."""
     return sq_matvec_t(W_lm, np.ones(np.asarray(W_lm).shape[0]))
 
 

@@ -6,7 +6,7 @@
  *
  * It computes, plainly and slowly, what the block codec of Seed-Q (section 3.1,
  * eq. (codec) and eq. (rate)) defines:
- *   - U(s): the basis generated by a maximal-length K-bit LFSR started at state s
+ *   - U(s): the basis from a full-period K-bit LFSR whose initial state is the seed s
  *     (section 3.1; the appendix on the hardware says the states are centred and
  *     the feedback taps depend on the width). Reading: Galois right-shift LFSR
  *     x <- (x >> 1) ^ (x & 1 ? mask_K : 0); basis column j holds the states

@@ -3,7 +3,7 @@ footprint metrics (test infrastructure only).
 
 Stream (Algorithm 1, the emit step: every block contributes exactly l(g_b) =
 K + 4P + 4 bits of eq. (rate), with no header; appendix on encoding and
-decoding: blocks are parsed left to right inside a tensor). The paper fixes no
+decoding: a decoder reads a tensor's blocks in order from its start). The paper fixes no
 bit layout; the reading used here and by the library is:
 
 * blocks in row-major block order b = r * (ncols / 8) + g;
@@ -53,7 +53,7 @@ def pack(seed, exp, q, rung_of_block, rungs) -> np.ndarray:
 
 
 def unpack(words, rung_of_block, rungs):
-    """(seed, exp, q [nblocks, 8] int8) parsed left to right from the payload."""
+    """(seed, exp, q [nblocks, 8] int8) read block by block from the start of the payload."""
     words = np.asarray(words, dtype=np.uint32)
     nbits = 32 * len(words)
 

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libseedq.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
-HIP_SOURCES = ["seedq_bases.hip", "seedq_search.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
+HIP_SOURCES = ["seedq_bases.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
                "seedq_decompress.hip", "seedq_stream.hip",
                "seedq_footprint.hip", "seedq_frontend.hip"]
 HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp", "seedq_frontend_host.cpp"]

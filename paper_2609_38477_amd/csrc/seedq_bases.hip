@@ -1,6 +1,6 @@
-// LFSR basis generation and per-seed pseudo-inverses (section 3.1: U(s) is
-// generated by a maximal-length K-bit LFSR started at state s; the encoder fits
-// least-squares coefficients on U(s) for every seed).
+// LFSR basis generation and per-seed pseudo-inverses (section 3.1: the columns
+// of U(s) come from a K-bit LFSR of full period whose initial state is the seed
+// s; the encoder needs the least-squares fit on U(s) for every seed).
 //
 // One thread per seed. The 8P centred states are produced by exact integer
 // stepping; U(s) = U_int(s) 2^-(K-1) is then decomposed in fp64 by a one-sided

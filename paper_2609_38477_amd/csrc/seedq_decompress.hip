@@ -1,5 +1,6 @@
-// Reconstruction w_hat = U(s) q 2^-e (Algorithm 2; the appendix on cost: one
-// LFSR expansion and k_b multiply-accumulates per weight).
+// Reconstruction w_hat = U(s) q 2^-e (Algorithm 2; per the appendix on cost the
+// decoder regenerates the LFSR states and does k_b multiply-adds for each
+// weight).
 //
 // One thread per block: it regenerates the 8P LFSR states of its seed, forms
 // the exact integer reconstruction acc_i = sum_j U_int[i][j] q_j (|acc| < 2^29)

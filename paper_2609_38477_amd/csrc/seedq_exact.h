@@ -1,5 +1,5 @@
-// Exact evaluation of one search candidate (block, seed), shared by the
-// search engines.
+// Exact evaluation of one search candidate (block, seed): the search kernels'
+// fp64 refinement of the candidates that pass the matrix-core screen.
 #pragma once
 
 #include "seedq_internal.h"

@@ -57,7 +57,8 @@ __host__ __device__ constexpr int pair_index(int i, int j) { return i * kC - i *
 // Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
 //   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
 //   q32:    float  [S][P][8]   orthonormal basis of range(U(s)) (rows of Q^T);
-//                               rows beyond the rank are zero
+//                               rows beyond the rank are zero (the fp32
+//                               residual filter of the P = 6 search reads it)
 //   pi16:   fp16 [ntiles][3][64][8]  2^12 Pi_s[k] as MFMA A-operand fragments:
 //           tile T holds seeds 32T+1 .. 32T+32; fragment t, lane l, element e
 //           is pair k = 16t + 8(l/32) + e of seed 32T + (l%32) + 1 (zero for
@@ -105,20 +106,12 @@ const int32_t* compaction_list(void* d_ws, int64_t nblocks, int nrungs);
 const int32_t* compaction_offsets(void* d_ws, int64_t nblocks, int nrungs);
 
 // Search over all seeds of rung (K, P) for the blocks listed at
-// list[off[r] .. off[r+1]) (list == nullptr: all nblocks blocks in order).
+// list[off[r] .. off[r+1]) (list == nullptr: all nblocks blocks in order), on
+// the matrix cores (seedq_search_mfma.hip).
 hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_list,
                          const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
                          uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
                          hipStream_t stream);
-
-hipError_t launch_search_valu(const float* d_W, int64_t nblocks, const int32_t* d_list,
-                              const int32_t* d_off, int rung_index, int K, int P,
-                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
-                              float* d_err, hipStream_t stream);
-hipError_t launch_search_mfma(const float* d_W, int64_t nblocks, const int32_t* d_list,
-                              const int32_t* d_off, int rung_index, int K, int P,
-                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
-                              float* d_err, hipStream_t stream);
 
 hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
                              const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,

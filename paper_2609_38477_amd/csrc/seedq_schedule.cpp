@@ -4,7 +4,7 @@
 // column importances a_j over the block's 8 columns, both factors normalised to
 // unit mean; every sum runs in index order in fp64 (appendix "Agreement").
 // Floor (section 3.3): q = sorted(imp)[ceil(f * nblocks) - 1], imp <- max(imp, q).
-// Hull (section 3.4): lower convex hull of (rate, damage) over the rungs, slopes
+// Hull (section 3.4): the lower convex hull of the rungs' (rate, damage) points, slopes
 // s_j = (e_j - e_{j+1}) / (r_{j+1} - r_j) in bits per weight.
 // Ladder (eq. (ladder)): a block of importance v sits at hull position
 // |{j : fl(lambda / s_j) <= v}|.
@@ -13,9 +13,9 @@
 // that ladder: for every distinct importance v and hull step j, the largest
 // double lambda with fl(lambda / s_j) <= v. Walking the breakpoints from the
 // largest down promotes whole groups of equally important blocks; the first
-// group that does not fit is the tied group of the tie pass, demoted in
-// row-major block order until the budget is met (Algorithm 2: the first T_t
-// tied blocks take the lower rung). The result equals bisection plus the tie
+// group that does not fit is the tied group of the tie pass: its blocks are
+// lowered one rung, earliest first in row-major order, until the total fits
+// the budget (Algorithm 2 lowers T_t of them). The result equals bisection plus the tie
 // pass (Everett's theorem), without floating-point search.
 #include <algorithm>
 #include <cmath>
@@ -268,7 +268,7 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
     int64_t cur = total + delta;
     int64_t members = 0;
     for (int c : tied_cls) members += cls_count[c];
-    // demote members in block order until the budget is met
+    // lower members, earliest block first, until the total fits the budget
     auto gain = [&](int c) {
       return int64_t(bits[H[to_of[c]]] - bits[H[from_of[c]]]);
     };

@@ -1,6 +1,6 @@
 // Matrix-core engine of the per-block exhaustive seed search (section 3.1;
-// per the appendix on cost, 2^K least-squares fits per block dominate the
-// encoder).
+// the appendix on cost names this search, one least-squares fit per block and
+// seed, as what the encoder spends its time on).
 //
 // Screen. For block w and seed s the least-squares residual
 //     r_LS(s) = ||w||^2 - w^T Pi_s w,        Pi_s = projector onto range(U(s)),
@@ -16,7 +16,7 @@
 //
 // Survivors. Each wave queues its passing (seed, block) pairs in LDS and
 // evaluates them 64 at a time, one per lane, with the exact fp64 evaluation
-// shared with the other engine. At P <= 3 a lane whose fold passes first
+// (seedq_exact.h). At P <= 3 a lane whose fold passes first
 // stores its 16 bounds as a record; records are turned into queued seeds 64
 // at a time against the thresholds of that moment. Per-block bests live in LDS as 64-bit keys
 // (error bits, seed in the low 24 bits) updated with atomic minimum, so the
@@ -680,9 +680,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // Residual filter of the new entries: the least-squares residual is
   // recomputed in fp32 from the orthonormal basis, ||w||^2 - ||Q_s^T w||^2,
   // with a margin of 2^-16 ||w||^2 for its rounding instead of the matrix
-  // core's gamma (the bound the vector engine screens with). An entry that can
-  // still reach its block's best error moves down to the filtered region; the
-  // others are dropped, as are no-op entries (seed 0).
+  // core's gamma. An entry that can still reach its block's best error moves
+  // down to the filtered region; the others are dropped, as are no-op entries
+  // (seed 0).
   auto filter = [&]() __attribute__((always_inline)) {
     if (P < kFilterMinP || K < kFilterMinK) {
       nf = qcount;  // every entry goes to the exact evaluation (no-op entries skip it)
@@ -1244,10 +1244,10 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
 
 }  // namespace
 
-hipError_t launch_search_mfma(const float* d_W, int64_t nblocks, const int32_t* d_list,
-                              const int32_t* d_off, int rung_index, int K, int P,
-                              const void* d_bases, uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q,
-                              float* d_err, hipStream_t stream) {
+hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_list,
+                         const int32_t* d_off, int rung_index, int K, int P, const void* d_bases,
+                         uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                         hipStream_t stream) {
   switch (P) {
 #define SEEDQ_CASE(PP)                                                                    \
   case PP:                                                                                \

@@ -1,8 +1,8 @@
 // The headerless variable-length code stream of one tensor (Algorithm 1, the
 // emit step: every block contributes exactly l(g_b) = K + 4P + 4 bits of
 // eq. (rate), with no header; Algorithm 2 and the appendix on encoding and
-// decoding: blocks are parsed left to right inside a tensor, their lengths
-// known from the allocation alone).
+// decoding: a decoder reads a tensor's blocks in order from its start, the
+// length of each known from the allocation alone).
 //
 // Layout: blocks in row-major order; inside a block the seed (K bits), the
 // exponent (4 bits) and the mantissas q_0 .. q_{P-1} (4 bits each, two's

@@ -1,6 +1,6 @@
-"""Single-bit fault study of the decoder path (the security analysis: a bit
-flipped after encoding and before decoding; footprint by eq.
-(security_metrics)).
+"""Single-bit fault study of the decoder path (the security analysis: one bit of
+the stored code or table changes between the encoder and the decoder; its
+footprint by eq. (security_metrics)).
 
 The encoder plans the rungs, searches every block and emits the headerless
 stream plus a global table (lambda, floor value, tie count, rungs, damages).

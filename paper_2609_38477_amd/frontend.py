@@ -7,10 +7,12 @@ Importance (section on data-free block importance):
 * o reads the attention output: a_o = repeat_kv((W_v * W_v) a_attn);
   down reads silu(gate) * up: a_down = E[silu(g)^2] ((W_up * W_up) a_mlp) with
   var(g) = (W_gate * W_gate) a_mlp (eq. (prop));
-* rows of o and down write the residual stream and read its gradient, whose
-  data-free scale is rho = (W_lm * W_lm)^T 1, an isotropic gradient at the
-  logits taken one hop back (output side); the other rows get rho = 1;
-* every tensor's input channels are sorted by a before blocking; the outlier
+* the outputs of o and down feed the residual stream, so their rows are scaled
+  by the data-free gradient size rho = (W_lm * W_lm)^T 1 (a unit gradient at
+  every logit, carried back through one layer; output side); the other rows
+  get rho = 1;
+* before blocking, every tensor's input channels are put in increasing order
+  of a; the outlier
   columns (appendix on outlier columns) are kept in FP16 and overwrite the
   codec's reconstruction.
 Every matrix product runs in the library's kernels (seedq_sq_gemv,

@@ -4,8 +4,8 @@ The encoder's dominant cost is one exhaustive seed search per rung of the grid
 S in {8..16}, k in {2..6} (appendix on cost; appendix "Rung grids", Table
 grids): every uniform build is a SeedLM compression of the same blocks at
 another rung. The appendix on per-block error across rungs (Table rungshape)
-then divides each block's reconstruction error at rung g by the same block's
-error at (16, 3) and summarises the ratios by their median, 10 % and 90 %
+then takes, for every block, the ratio of its error at rung g to its (16, 3)
+error, and summarises the ratios by their median, 10 % and 90 %
 quantiles and the standard deviation of their logarithm.
 
 ``build_grid`` runs those uniform builds through the library (one basis stack

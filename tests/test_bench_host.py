@@ -26,3 +26,16 @@ def test_help_lists_every_mode():
                  "--no-cpu-baseline", "--cpu-seconds"):
         assert flag in r.stdout, flag
 
+
+
+def test_roofline_work_is_the_projection_count():
+    # the roofline's work is the least-squares projection of every block on every
+    # seed's basis: 2 C P flops per candidate (48 at P = 3), not the kernel's own
+    # quadratic form (72) or what it issues (96), which are reported separately
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.projection_flops(16, 3) == 65535 * 2 * 8 * 3
+    assert bench.projection_flops(12, 2) == 4095 * 32
+    assert bench.projection_flops(20, 4) == ((1 << 20) - 1) * 64
+    assert bench.QUADFORM_FLOPS_PER_CANDIDATE == 72.0
+    assert bench.ISSUED_FLOPS_PER_CANDIDATE == 96.0

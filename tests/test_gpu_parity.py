@@ -5,9 +5,9 @@ Bars (written out in each test):
   - search: for every checked block the oracle's exact error of the GPU's code
     is within 1e-5 relative of the oracle's best (plus 1e-7 ||w||^2 for
     zero-error blocks, which must match exactly); the GPU's reported error is
-    the oracle's error of that code to fp32 rounding; seeds agree on >= 99.9 %
-    of blocks up to ties at the resolution of the search's ordering key
-    (2^-28 relative), and every disagreement is within the 1e-5 bar.
+    the oracle's error of that code to fp32 rounding; the chosen seed is the
+    oracle's on >= 99.9 % of the checked blocks, and every block whose seed
+    differs is a near-tie within the 1e-5 bar.
 """
 import numpy as np
 import pytest
@@ -56,11 +56,11 @@ def check_search(oq, blocks, K, P, seed, e, q, err, label=""):
     # reported error is the exact error of the reported code, rounded to fp32
     assert np.all(np.abs(err - mine) <= 1e-6 * mine + 1e-30), label
     same = seed == ref.seed
-    # a different seed is allowed only where the errors tie to the resolution of
-    # the search's ordering key (2^-28 relative); elsewhere seeds must agree on
-    # >= 99.9 % of blocks
-    key_tie = mine <= ref.err * (1 + 2.0 ** -26)
-    assert (same | key_tie).mean() >= 0.999, f"{label}: seed agreement {same.mean():.5f}"
+    # the oracle's seed on at least 99.9 % of the checked blocks
+    assert same.mean() >= 0.999, f"{label}: seed agreement {same.mean():.5f}"
+    # every other block is a near-tie: its code is within the 1e-5 bar (checked
+    # above for all blocks, repeated here for the disagreements by name)
+    assert np.all(mine[~same] <= ref.err[~same] * (1 + REL) + TAU * ww[~same]), label
     # where seeds agree the codes are identical
     assert np.array_equal(e[same], ref.e[same]) and np.array_equal(q[same], ref.q[same]), label
     zero = ref.err == 0.0
@@ -322,8 +322,10 @@ def test_search_deterministic(sq, torch):
 
 
 def test_search_k20_sampled(sq, oq, torch):
+    # 64 blocks at (20, 4): sequential seed chunks, concurrent ranges and the
+    # rebuilding kernel's record stage, against the oracle's exhaustive search
     K, P = 20, 4
-    W = synthetic.weights(1, 8 * 12, 0.02, key=20, outlier_frac=0.02)
+    W = synthetic.weights(1, 8 * 64, 0.02, key=20, outlier_frac=0.02)
     b = sq.build_bases(K, P)
     seed, e, q, err = sq.compress(_dev(torch, W), [b])
     torch.cuda.synchronize()
@@ -537,7 +539,7 @@ def test_seed_bit_flip_footprint(sq, torch):
 def test_search_full_size_three_rungs_sampled(sq, oq, torch, name):
     # 4096 x 11008 at 3.5 bits per weight, 4096 x 14336 and 8192 x 28672 at 4.0,
     # over (12,2)/(16,3)/(20,4), with the schedule, compaction and one search
-    # launch per rung exactly as the benchmark runs them; the oracle checks
+    # launch per rung exactly as the benchmark runs them; the oracle checks 512
     # evenly spaced blocks of every rung
     wl = synthetic.WORKLOADS[name]
     W = synthetic.workload_weights(wl)
@@ -557,7 +559,7 @@ def test_search_full_size_three_rungs_sampled(sq, oq, torch, name):
         sel = np.nonzero(rob == r)[0]
         assert np.all((seed[sel] >= 1) & (seed[sel] < (1 << K)))
         assert not q[sel][:, P:].any()
-        n = 64 if K == 20 else 512
+        n = 512
         idx = sel[np.linspace(0, len(sel) - 1, n).astype(np.int64)]
         check_search(oq, blocks[idx].astype(np.float32), K, P, seed[idx], e[idx], q[idx], err[idx],
                      f"{name} rung{r}")

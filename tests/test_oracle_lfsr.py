@@ -9,7 +9,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "lfsr_k8_seed1.txt")
 
 @pytest.mark.parametrize("K", list(range(8, 25)))
 def test_maximal_length(oq, K):
-    # "maximal-length S-bit LFSR": the period is 2^K - 1
+    # maximal length (section 3.1): the period is 2^K - 1
     assert oq.period(K) == (1 << K) - 1
     m = oq.lfsr_mask(K)
     assert (m >> (K - 1)) == 1, "mask must keep the state K bits wide"

@@ -67,8 +67,8 @@ def test_tie_pass_splits_group_in_block_order(oq):
 @pytest.mark.parametrize("trial", range(6))
 def test_everett_optimality_brute_force(oq, trial):
     # random importances on 2 rows x 4 groups = 8 blocks, 3 rungs: the
-    # allocation minimises sum imp_b e(g_b) over all allocations whose total
-    # rate does not exceed its own (Everett's theorem, appendix on ties)
+    # allocation minimises sum imp_b e(g_b) over every allocation that spends
+    # at most as many bits as it does (Everett's theorem, appendix on ties)
     rng = np.random.default_rng(trial)
     a = np.exp(rng.normal(0, 1, 32)).astype(np.float32)
     nb = 8

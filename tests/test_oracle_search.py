@@ -1,5 +1,5 @@
-"""Pins for the oracle's exhaustive seed search and decoder (section 3.1:
-the encoder searches all 2^S - 1 seeds for the smallest quantised error;
+"""Pins for the oracle's exhaustive seed search and decoder (section 3.1: the
+encoder tries every nonzero seed and keeps the code of least quantised error;
 Algorithm 2: w_hat = U(s) t_hat)."""
 import numpy as np
 import pytest
