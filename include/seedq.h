@@ -196,13 +196,12 @@ size_t seedq_compress_workspace_bytes(int64_t nrows, int64_t ncols, int32_t C, i
  * A block whose 8 weights are all zero gets seed 1, e = 15, q = 0, err = 0 (every
  * seed ties). Asynchronous on hip_stream.
  * For K >= 17 the seed tiles are searched in sequential chunks of 2048 tiles
- * (one launch each), and the seeds of a rung with too few blocks to fill the
- * GPU are searched in several parts at once; in either case, until the call
- * completes, d_q holds each block's best 64-bit ordering key so far (d_q must
- * be 8-byte aligned, as for every call). The result is the same for every split. The environment
- * variables SEEDQ_SEED_CHUNK_TILES (tiles per chunk, 0 = one chunk) and
- * SEEDQ_SEED_SPLITS (parts at once, 1 = one), read at each call, override the
- * choice (clamped to at most 256 parts and at least 8 seed tiles per part).
+ * (one launch each); until the call completes, d_q holds each block's best
+ * exact error so far (its fp64 bit pattern; d_q must be 8-byte aligned, as for
+ * every call) and d_seed the seed of that error. The result is the same for
+ * every chunk length: the smallest exact error, ties to the smallest seed. The
+ * environment variable SEEDQ_SEED_CHUNK_TILES (tiles per chunk, 0 = one chunk),
+ * read at each call, overrides the choice (at least 8 seed tiles per chunk).
  * Errors: SEEDQ_EINVAL, SEEDQ_EUNSUPPORTED, SEEDQ_EWORKSPACE, SEEDQ_EHIP.
  */
 int seedq_compress(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
@@ -342,9 +341,9 @@ int seedq_footprint(const float* d_clean, const float* d_corrupt, int64_t n, lon
  * ---- Data-free importance front end (section on data-free block importance:
  * eq. (gamma), eq. (prop), the output-side rho and the channel sort; appendix
  * on outlier columns). The caller composes these into the a_j and rho_r that
- * seedq_schedule_desc takes: a_j = gamma_j^2 for the projections that read
- * gamma * RMSNorm(h); a_o = repeat_kv(sq_gemv(W_v, a_in)); a_down = E[silu(g)^2] *
- * sq_gemv(W_up, a_in) with var(g) = sq_gemv(W_gate, a_in); rho = sq_gemv^T(W_lm, 1).
+ * seedq_schedule_desc takes: a_j = gamma_j^2 (seedq_gamma_importance) for the
+ * projections that read gamma * RMSNorm(h); a_o (seedq_propagate_o) and a_down
+ * (seedq_propagate_down) one hop further; rho = sq_gemv^T(W_lm, 1).
  */
 
 /* Gauss-Hermite rule with n nodes (1 <= n <= 256) for the weight e^{-x^2}: nodes
@@ -380,6 +379,48 @@ int seedq_column_stats(const float* d_W, int64_t nrows, int64_t ncols, double* d
  * fp64. Asynchronous on hip_stream. Errors: SEEDQ_EINVAL, SEEDQ_EHIP. */
 int seedq_expect_silu_sq(const double* d_var, int64_t n, int32_t nodes, double* d_out,
                          void* hip_stream);
+
+/* a_j = gamma_j^2 (eq. (gamma)): the importance of the input channels of the
+ * projections that read gamma * RMSNorm(h) (q, k, v from the attention norm;
+ * gate, up from the MLP norm). d_gamma: device fp32 [n]; d_a: device fp64 [n]
+ * out (exact: the square of an fp32 value fits in fp64). Asynchronous on
+ * hip_stream. Errors: SEEDQ_EINVAL, SEEDQ_EHIP. */
+int seedq_gamma_importance(const float* d_gamma, int64_t n, double* d_a, void* hip_stream);
+
+/* Workspace bytes of seedq_propagate_o and seedq_propagate_down for a weight of
+ * nrows x ncols (a_in in fp32 and one fp64 per row); 0 for a bad shape. */
+size_t seedq_propagate_workspace_bytes(int64_t nrows, int64_t ncols);
+
+/* One-hop propagation to the input of o (eq. (prop)): o reads the attention
+ * output, whose channel h * head_dim + i comes from the value row
+ * (h / (n_heads / n_kv_heads)) * head_dim + i, so
+ *   a_o = repeat_kv((W_v * W_v) a_in),
+ * the n_kv_heads blocks of head_dim = nrows / n_kv_heads rows each repeated for
+ * the n_heads / n_kv_heads (at most 64) query heads that share them, head-major.
+ *   d_Wv: device fp32 [nrows][ncols] (16-byte aligned, ncols % 4 == 0).
+ *   d_a_in: device fp64 [ncols], the importance of W_v's input channels; it
+ *           enters the products rounded to fp32 (stored factors are single
+ *           precision, the appendix on agreement); products and sums in fp64.
+ *   d_a_o: device fp64 [n_heads * head_dim] out.
+ *   d_workspace: seedq_propagate_workspace_bytes(nrows, ncols) bytes, 256-byte aligned.
+ * Asynchronous on hip_stream. Errors: SEEDQ_EINVAL, SEEDQ_EWORKSPACE, SEEDQ_EHIP. */
+int seedq_propagate_o(const float* d_Wv, int64_t nrows, int64_t ncols, int32_t n_heads,
+                      int32_t n_kv_heads, const double* d_a_in, double* d_a_o, void* d_workspace,
+                      size_t workspace_bytes, void* hip_stream);
+
+/* One-hop propagation to the input of down (eq. (prop)): down reads
+ * silu(gate x) * (up x), so
+ *   a_down = E[silu(g)^2] * ((W_up * W_up) a_in),  g ~ N(0, (W_gate * W_gate) a_in),
+ * the expectation by the nodes-point Gauss-Hermite rule of seedq_gauss_hermite
+ * (1 <= nodes <= 128), everything in fp64.
+ *   d_Wgate, d_Wup: device fp32 [nrows][ncols] each (16-byte aligned, ncols % 4 == 0).
+ *   d_a_in: device fp64 [ncols] (rounded to fp32 before the products, as for o).
+ *   d_a_down: device fp64 [nrows] out.
+ *   d_workspace: seedq_propagate_workspace_bytes(nrows, ncols) bytes, 256-byte aligned.
+ * Asynchronous on hip_stream. Errors: SEEDQ_EINVAL, SEEDQ_EWORKSPACE, SEEDQ_EHIP. */
+int seedq_propagate_down(const float* d_Wgate, const float* d_Wup, int64_t nrows, int64_t ncols,
+                         const double* d_a_in, int32_t nodes, double* d_a_down, void* d_workspace,
+                         size_t workspace_bytes, void* hip_stream);
 
 /* Channel sort before blocking: perm[k] = the input channel placed k-th, in
  * increasing a, ties by channel index (host arrays of n). Host only.

@@ -121,6 +121,14 @@ def lib() -> ctypes.CDLL:
         L.seedq_column_stats.argtypes = [vp, i64, i64, vp, vp, vp]
         L.seedq_expect_silu_sq.restype = ctypes.c_int
         L.seedq_expect_silu_sq.argtypes = [vp, i64, i32, vp, vp]
+        L.seedq_gamma_importance.restype = ctypes.c_int
+        L.seedq_gamma_importance.argtypes = [vp, i64, vp, vp]
+        L.seedq_propagate_workspace_bytes.restype = sz
+        L.seedq_propagate_workspace_bytes.argtypes = [i64, i64]
+        L.seedq_propagate_o.restype = ctypes.c_int
+        L.seedq_propagate_o.argtypes = [vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
+        L.seedq_propagate_down.restype = ctypes.c_int
+        L.seedq_propagate_down.argtypes = [vp, vp, i64, i64, vp, i32, vp, vp, sz, vp]
         L.seedq_channel_order.restype = ctypes.c_int
         L.seedq_channel_order.argtypes = [vp, i64, vp]
         L.seedq_permute_columns.restype = ctypes.c_int
@@ -301,6 +309,29 @@ def seedq_column_stats(d_W, nrows: int, ncols: int, d_maxabs, d_median, stream=N
 def seedq_expect_silu_sq(d_var, n: int, nodes: int, d_out, stream=None) -> None:
     _check(lib().seedq_expect_silu_sq(_ptr(d_var), n, nodes, _ptr(d_out), _stream(stream)),
            "seedq_expect_silu_sq")
+
+
+def seedq_gamma_importance(d_gamma, n: int, d_a, stream=None) -> None:
+    _check(lib().seedq_gamma_importance(_ptr(d_gamma), n, _ptr(d_a), _stream(stream)),
+           "seedq_gamma_importance")
+
+
+def seedq_propagate_workspace_bytes(nrows: int, ncols: int) -> int:
+    return int(lib().seedq_propagate_workspace_bytes(nrows, ncols))
+
+
+def seedq_propagate_o(d_Wv, nrows: int, ncols: int, n_heads: int, n_kv_heads: int, d_a_in, d_a_o,
+                      d_workspace, workspace_bytes: int, stream=None) -> None:
+    _check(lib().seedq_propagate_o(_ptr(d_Wv), nrows, ncols, n_heads, n_kv_heads, _ptr(d_a_in),
+                                   _ptr(d_a_o), _ptr(d_workspace), workspace_bytes,
+                                   _stream(stream)), "seedq_propagate_o")
+
+
+def seedq_propagate_down(d_Wgate, d_Wup, nrows: int, ncols: int, d_a_in, nodes: int, d_a_down,
+                         d_workspace, workspace_bytes: int, stream=None) -> None:
+    _check(lib().seedq_propagate_down(_ptr(d_Wgate), _ptr(d_Wup), nrows, ncols, _ptr(d_a_in), nodes,
+                                      _ptr(d_a_down), _ptr(d_workspace), workspace_bytes,
+                                      _stream(stream)), "seedq_propagate_down")
 
 
 def seedq_channel_order(a) -> np.ndarray:

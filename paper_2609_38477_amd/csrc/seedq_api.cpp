@@ -16,6 +16,47 @@ bool shape_ok(int64_t nrows, int64_t ncols) {
 
 }  // namespace
 
+namespace seedq {
+
+int check_compress_args(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
+                        const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
+                        const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q) {
+  if (C != kC) return SEEDQ_EUNSUPPORTED;
+  if (!d_W || !bases || !d_seed || !d_exp || !d_q) return SEEDQ_EINVAL;
+  if (!shape_ok(nrows, ncols) || nrungs < 1 || nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_W) & 31u || reinterpret_cast<uintptr_t>(d_q) & 7u)
+    return SEEDQ_EINVAL;
+  for (int r = 0; r < nrungs; ++r) {
+    if (!rung_supported(bases[r].K, bases[r].P)) return SEEDQ_EUNSUPPORTED;
+    if (!bases[r].d_bases) return SEEDQ_EINVAL;
+  }
+  if (nrungs > 1 && !d_rung_of_block) return SEEDQ_EINVAL;
+  return SEEDQ_OK;
+}
+
+int run_compress(const float* d_W, int64_t nrows, int64_t ncols, const uint8_t* d_rung_of_block,
+                 int32_t nrungs, const seedq_bases* bases, uint32_t* d_seed, uint8_t* d_exp,
+                 int8_t* d_q, float* d_err, void* d_workspace, hipStream_t stream) {
+  const int64_t nb = nrows * (ncols / kC);
+  if (nrungs == 1) {
+    const hipError_t e = launch_search(d_W, nb, nullptr, nullptr, 0, bases[0].K, bases[0].P,
+                                       bases[0].d_bases, d_seed, d_exp, d_q, d_err, stream);
+    return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+  }
+  hipError_t e = launch_compaction(d_rung_of_block, nb, nrungs, d_workspace, d_seed, stream);
+  if (e != hipSuccess) return SEEDQ_EHIP;
+  const int32_t* list = compaction_list(d_workspace, nb, nrungs);
+  const int32_t* off = compaction_offsets(d_workspace, nb, nrungs);
+  for (int r = 0; r < nrungs; ++r) {
+    e = launch_search(d_W, nb, list, off, r, bases[r].K, bases[r].P, bases[r].d_bases, d_seed,
+                      d_exp, d_q, d_err, stream);
+    if (e != hipSuccess) return SEEDQ_EHIP;
+  }
+  return SEEDQ_OK;
+}
+
+}  // namespace seedq
+
 extern "C" {
 
 const char* seedq_strerror(int code) {
@@ -66,36 +107,17 @@ int seedq_compress(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
                    const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
                    uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
                    void* d_workspace, size_t workspace_bytes, void* hip_stream) {
-  if (C != kC) return SEEDQ_EUNSUPPORTED;
-  if (!d_W || !bases || !d_seed || !d_exp || !d_q) return SEEDQ_EINVAL;
-  if (!shape_ok(nrows, ncols) || nrungs < 1 || nrungs > SEEDQ_MAX_RUNGS) return SEEDQ_EINVAL;
-  if (reinterpret_cast<uintptr_t>(d_W) & 31u || reinterpret_cast<uintptr_t>(d_q) & 7u)
-    return SEEDQ_EINVAL;
-  for (int r = 0; r < nrungs; ++r) {
-    if (!rung_supported(bases[r].K, bases[r].P)) return SEEDQ_EUNSUPPORTED;
-    if (!bases[r].d_bases) return SEEDQ_EINVAL;
+  const int rc = check_compress_args(d_W, nrows, ncols, C, d_rung_of_block, nrungs, bases, d_seed,
+                                     d_exp, d_q);
+  if (rc != SEEDQ_OK) return rc;
+  if (nrungs > 1) {
+    const size_t need = compaction_workspace_bytes(nrows * (ncols / kC), nrungs);
+    if (!d_workspace || workspace_bytes < need ||
+        (reinterpret_cast<uintptr_t>(d_workspace) & 255u))
+      return SEEDQ_EWORKSPACE;
   }
-  if (nrungs > 1 && !d_rung_of_block) return SEEDQ_EINVAL;
-  const int64_t nb = nrows * (ncols / kC);
-  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  if (nrungs == 1) {
-    const hipError_t e = launch_search(d_W, nb, nullptr, nullptr, 0, bases[0].K, bases[0].P,
-                                       bases[0].d_bases, d_seed, d_exp, d_q, d_err, stream);
-    return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
-  }
-  const size_t need = compaction_workspace_bytes(nb, nrungs);
-  if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255u))
-    return SEEDQ_EWORKSPACE;
-  hipError_t e = launch_compaction(d_rung_of_block, nb, nrungs, d_workspace, d_seed, stream);
-  if (e != hipSuccess) return SEEDQ_EHIP;
-  const int32_t* list = compaction_list(d_workspace, nb, nrungs);
-  const int32_t* off = compaction_offsets(d_workspace, nb, nrungs);
-  for (int r = 0; r < nrungs; ++r) {
-    e = launch_search(d_W, nb, list, off, r, bases[r].K, bases[r].P, bases[r].d_bases, d_seed,
-                      d_exp, d_q, d_err, stream);
-    if (e != hipSuccess) return SEEDQ_EHIP;
-  }
-  return SEEDQ_OK;
+  return run_compress(d_W, nrows, ncols, d_rung_of_block, nrungs, bases, d_seed, d_exp, d_q, d_err,
+                      d_workspace, static_cast<hipStream_t>(hip_stream));
 }
 
 int seedq_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
@@ -301,8 +323,64 @@ int seedq_expect_silu_sq(const double* d_var, int64_t n, int32_t nodes, double* 
   double x[128], w[128];
   const int rc = gauss_hermite(nodes, x, w);
   if (rc != SEEDQ_OK) return rc;
+  const hipError_t e = launch_expect_silu_sq(d_var, n, nodes, x, w, nullptr, d_out,
+                                             static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_gamma_importance(const float* d_gamma, int64_t n, double* d_a, void* hip_stream) {
+  if (!d_gamma || !d_a || n < 0) return SEEDQ_EINVAL;
+  if (n == 0) return SEEDQ_OK;
+  const hipError_t e = launch_gamma_importance(d_gamma, n, d_a, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+size_t seedq_propagate_workspace_bytes(int64_t nrows, int64_t ncols) {
+  if (nrows <= 0 || ncols <= 0) return 0;
+  return propagate_workspace_bytes(nrows, ncols);
+}
+
+namespace {
+
+int propagate_args(const float* d_W, int64_t nrows, int64_t ncols, const double* d_a_in,
+                   const double* d_out, void* d_ws, size_t ws_bytes) {
+  if (!d_W || !d_a_in || !d_out || nrows <= 0 || ncols <= 0 || (ncols & 3)) return SEEDQ_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_W) & 15u) return SEEDQ_EINVAL;
+  if (!d_ws || ws_bytes < propagate_workspace_bytes(nrows, ncols) ||
+      (reinterpret_cast<uintptr_t>(d_ws) & 255u))
+    return SEEDQ_EWORKSPACE;
+  return SEEDQ_OK;
+}
+
+}  // namespace
+
+int seedq_propagate_o(const float* d_Wv, int64_t nrows, int64_t ncols, int32_t n_heads,
+                      int32_t n_kv_heads, const double* d_a_in, double* d_a_o, void* d_workspace,
+                      size_t workspace_bytes, void* hip_stream) {
+  if (n_kv_heads < 1 || n_heads < n_kv_heads || n_heads % n_kv_heads || nrows % n_kv_heads ||
+      n_heads / n_kv_heads > 64)
+    return SEEDQ_EINVAL;
+  const int rc = propagate_args(d_Wv, nrows, ncols, d_a_in, d_a_o, d_workspace, workspace_bytes);
+  if (rc != SEEDQ_OK) return rc;
+  const hipError_t e = launch_propagate_o(d_Wv, nrows, ncols, n_heads, n_kv_heads, d_a_in, d_a_o,
+                                          d_workspace, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
+}
+
+int seedq_propagate_down(const float* d_Wgate, const float* d_Wup, int64_t nrows, int64_t ncols,
+                         const double* d_a_in, int32_t nodes, double* d_a_down, void* d_workspace,
+                         size_t workspace_bytes, void* hip_stream) {
+  if (!d_Wup || (reinterpret_cast<uintptr_t>(d_Wup) & 15u) || nodes < 1 || nodes > 128)
+    return SEEDQ_EINVAL;
+  const int rc =
+      propagate_args(d_Wgate, nrows, ncols, d_a_in, d_a_down, d_workspace, workspace_bytes);
+  if (rc != SEEDQ_OK) return rc;
+  double x[128], w[128];
+  const int grc = gauss_hermite(nodes, x, w);
+  if (grc != SEEDQ_OK) return grc;
   const hipError_t e =
-      launch_expect_silu_sq(d_var, n, nodes, x, w, d_out, static_cast<hipStream_t>(hip_stream));
+      launch_propagate_down(d_Wgate, d_Wup, nrows, ncols, d_a_in, nodes, x, w, d_a_down,
+                            d_workspace, static_cast<hipStream_t>(hip_stream));
   return e == hipSuccess ? SEEDQ_OK : SEEDQ_EHIP;
 }
 

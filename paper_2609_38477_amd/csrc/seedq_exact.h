@@ -67,16 +67,4 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
   return err;
 }
 
-// Ordering key of a candidate: the fp64 error with its low 24 mantissa bits
-// replaced by the seed. Keys order candidates by error to 2^-28 relative and,
-// among errors equal to that resolution, by seed; err >= 0, so the unsigned
-// order of the bits is the numeric order.
-__device__ __forceinline__ uint64_t candidate_key(double err, uint32_t seed) {
-  return (uint64_t(__double_as_longlong(err)) & ~uint64_t(0xFFFFFF)) | uint64_t(seed);
-}
-
-__device__ __forceinline__ double key_error(uint64_t key) {
-  return __longlong_as_double((long long)(key & ~uint64_t(0xFFFFFF)));
-}
-
 }  // namespace seedq

@@ -29,10 +29,13 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
-// One wave per row; lanes take 4 consecutive columns at a time.
+// One wave per row; lanes take 4 consecutive columns at a time. Row r's sum
+// goes to out[(r / hd * group + g) * hd + r % hd] for g < group: group = 1,
+// hd = nrows is the plain product; group > 1 repeats each block of hd rows
+// (one key-value head) for the group query heads that share it, head-major.
 __global__ void __launch_bounds__(kThreads)
 sq_gemv_kernel(const float* __restrict__ W, int64_t nrows, int64_t ncols,
-               const float* __restrict__ v, double* __restrict__ out) {
+               const float* __restrict__ v, int64_t hd, int group, double* __restrict__ out) {
   const int64_t r = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
   if (r >= nrows) return;
   const int lane = threadIdx.x & 63;
@@ -47,7 +50,24 @@ sq_gemv_kernel(const float* __restrict__ W, int64_t nrows, int64_t ncols,
     acc += double(w.w) * double(w.w) * double(x.w);
   }
   acc = wave_sum(acc);
-  if (lane == 0) out[r] = acc;
+  const int64_t head = r / hd, i = r - head * hd;
+  if (lane < group) out[(head * group + lane) * hd + i] = acc;
+}
+
+// a_j = gamma_j^2 in fp64 (exact: the square of an fp32 value fits in 48 bits).
+__global__ void __launch_bounds__(kThreads)
+gamma_sq_kernel(const float* __restrict__ g, int64_t n, double* __restrict__ a) {
+  const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const double x = double(g[i]);
+  a[i] = x * x;
+}
+
+// Importance factors enter the products in single precision (round to nearest).
+__global__ void __launch_bounds__(kThreads)
+to_f32_kernel(const double* __restrict__ in, int64_t n, float* __restrict__ out) {
+  const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (i < n) out[i] = float(in[i]);
 }
 
 constexpr int kRowChunk = 256;
@@ -159,9 +179,10 @@ struct GaussHermite {
   double x[128], w[128];
 };
 
+// out[i] = E[silu(g)^2], g ~ N(0, var[i]), times scale[i] when scale is given.
 __global__ void __launch_bounds__(kThreads)
 expect_silu_sq_kernel(const double* __restrict__ var, int64_t n, GaussHermite gh,
-                      double* __restrict__ out) {
+                      const double* __restrict__ scale, double* __restrict__ out) {
   const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (i >= n) return;
   const double s = sqrt(2.0 * var[i]);
@@ -171,7 +192,8 @@ expect_silu_sq_kernel(const double* __restrict__ var, int64_t n, GaussHermite gh
     const double silu = g / (1.0 + exp(-g));
     acc += gh.w[k] * silu * silu;
   }
-  out[i] = acc / sqrt(3.14159265358979323846);
+  const double e = acc / sqrt(3.14159265358979323846);
+  out[i] = scale ? e * scale[i] : e;
 }
 
 // out[r][j] = in[r][perm[j]] (gather) or out[r][perm[j]] = in[r][j] (scatter);
@@ -228,7 +250,7 @@ hipError_t launch_sq_gemv(const float* d_W, int64_t nrows, int64_t ncols, const 
   if (!transpose) {
     const unsigned grid = unsigned((nrows + kThreads / 64 - 1) / (kThreads / 64));
     hipLaunchKernelGGL(sq_gemv_kernel, dim3(grid), dim3(kThreads), 0, stream, d_W, nrows, ncols,
-                       d_v, d_out);
+                       d_v, nrows, 1, d_out);
     return hipGetLastError();
   }
   const int64_t nchunks = (nrows + kRowChunk - 1) / kRowChunk;
@@ -250,7 +272,8 @@ hipError_t launch_column_stats(const float* d_W, int64_t nrows, int64_t ncols, d
 }
 
 hipError_t launch_expect_silu_sq(const double* d_var, int64_t n, int nodes, const double* x,
-                                 const double* w, double* d_out, hipStream_t stream) {
+                                 const double* w, const double* d_scale, double* d_out,
+                                 hipStream_t stream) {
   GaussHermite gh;
   gh.n = nodes;
   for (int k = 0; k < nodes; ++k) {
@@ -259,8 +282,51 @@ hipError_t launch_expect_silu_sq(const double* d_var, int64_t n, int nodes, cons
   }
   const unsigned grid = unsigned((n + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(expect_silu_sq_kernel, dim3(grid), dim3(kThreads), 0, stream, d_var, n, gh,
-                     d_out);
+                     d_scale, d_out);
   return hipGetLastError();
+}
+
+hipError_t launch_gamma_importance(const float* d_gamma, int64_t n, double* d_a,
+                                   hipStream_t stream) {
+  const unsigned grid = unsigned((n + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(gamma_sq_kernel, dim3(grid), dim3(kThreads), 0, stream, d_gamma, n, d_a);
+  return hipGetLastError();
+}
+
+// Workspace of the propagation calls: a_in in fp32 [ncols] and var(g) [nrows].
+size_t propagate_workspace_bytes(int64_t nrows, int64_t ncols) {
+  return align256(sizeof(float) * size_t(ncols)) + align256(sizeof(double) * size_t(nrows));
+}
+
+hipError_t launch_propagate_o(const float* d_Wv, int64_t nrows, int64_t ncols, int n_heads,
+                              int n_kv_heads, const double* d_a_in, double* d_a_o, void* d_ws,
+                              hipStream_t stream) {
+  float* a32 = static_cast<float*>(d_ws);
+  hipLaunchKernelGGL(to_f32_kernel, dim3(unsigned((ncols + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, stream, d_a_in, ncols, a32);
+  const unsigned grid = unsigned((nrows + kThreads / 64 - 1) / (kThreads / 64));
+  hipLaunchKernelGGL(sq_gemv_kernel, dim3(grid), dim3(kThreads), 0, stream, d_Wv, nrows, ncols,
+                     static_cast<const float*>(a32), nrows / n_kv_heads, n_heads / n_kv_heads,
+                     d_a_o);
+  return hipGetLastError();
+}
+
+hipError_t launch_propagate_down(const float* d_Wgate, const float* d_Wup, int64_t nrows,
+                                 int64_t ncols, const double* d_a_in, int nodes, const double* x,
+                                 const double* w, double* d_a_down, void* d_ws,
+                                 hipStream_t stream) {
+  float* a32 = static_cast<float*>(d_ws);
+  double* var = reinterpret_cast<double*>(static_cast<char*>(d_ws) +
+                                          align256(sizeof(float) * size_t(ncols)));
+  hipLaunchKernelGGL(to_f32_kernel, dim3(unsigned((ncols + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, stream, d_a_in, ncols, a32);
+  const unsigned grid = unsigned((nrows + kThreads / 64 - 1) / (kThreads / 64));
+  hipLaunchKernelGGL(sq_gemv_kernel, dim3(grid), dim3(kThreads), 0, stream, d_Wgate, nrows, ncols,
+                     static_cast<const float*>(a32), nrows, 1, var);
+  hipLaunchKernelGGL(sq_gemv_kernel, dim3(grid), dim3(kThreads), 0, stream, d_Wup, nrows, ncols,
+                     static_cast<const float*>(a32), nrows, 1, d_a_down);
+  // a_down = E[silu(g)^2] * up, with up already in d_a_down (read before written, per element)
+  return launch_expect_silu_sq(var, nrows, nodes, x, w, d_a_down, d_a_down, stream);
 }
 
 hipError_t launch_permute_columns(const float* d_in, int64_t nrows, int64_t ncols,

@@ -113,6 +113,17 @@ hipError_t launch_search(const float* d_W, int64_t nblocks, const int32_t* d_lis
                          uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
                          hipStream_t stream);
 
+// seedq_compress without its workspace checks (seedq_api.cpp): argument checks
+// shared by the compress entry points, then the compaction (nrungs > 1, in
+// d_workspace, 256-byte aligned and at least compaction_workspace_bytes) and one
+// search per rung. SEEDQ_OK or an error code.
+int check_compress_args(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
+                        const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
+                        const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q);
+int run_compress(const float* d_W, int64_t nrows, int64_t ncols, const uint8_t* d_rung_of_block,
+                 int32_t nrungs, const seedq_bases* bases, uint32_t* d_seed, uint8_t* d_exp,
+                 int8_t* d_q, float* d_err, void* d_workspace, hipStream_t stream);
+
 hipError_t launch_decompress(const uint32_t* d_seed, const uint8_t* d_exp, const int8_t* d_q,
                              const uint8_t* d_rung, const RungTable& rt, int64_t nblocks,
                              float* d_W_hat, int32_t* d_acc, hipStream_t stream);
@@ -148,7 +159,18 @@ hipError_t launch_sq_gemv(const float* d_W, int64_t nrows, int64_t ncols, const 
 hipError_t launch_column_stats(const float* d_W, int64_t nrows, int64_t ncols, double* d_max,
                                double* d_median, hipStream_t stream);
 hipError_t launch_expect_silu_sq(const double* d_var, int64_t n, int nodes, const double* x,
-                                 const double* w, double* d_out, hipStream_t stream);
+                                 const double* w, const double* d_scale, double* d_out,
+                                 hipStream_t stream);
+hipError_t launch_gamma_importance(const float* d_gamma, int64_t n, double* d_a,
+                                   hipStream_t stream);
+size_t propagate_workspace_bytes(int64_t nrows, int64_t ncols);
+hipError_t launch_propagate_o(const float* d_Wv, int64_t nrows, int64_t ncols, int n_heads,
+                              int n_kv_heads, const double* d_a_in, double* d_a_o, void* d_ws,
+                              hipStream_t stream);
+hipError_t launch_propagate_down(const float* d_Wgate, const float* d_Wup, int64_t nrows,
+                                 int64_t ncols, const double* d_a_in, int nodes, const double* x,
+                                 const double* w, double* d_a_down, void* d_ws,
+                                 hipStream_t stream);
 hipError_t launch_permute_columns(const float* d_in, int64_t nrows, int64_t ncols,
                                   const int32_t* d_perm, int inverse, float* d_out,
                                   hipStream_t stream);

@@ -16,21 +16,22 @@
 //
 // Survivors. Each wave queues its passing (seed, block) pairs in LDS and
 // evaluates them 64 at a time, one per lane, with the exact fp64 evaluation
-// (seedq_exact.h). At P <= 3 a lane whose fold passes first
-// stores its 16 bounds as a record; records are turned into queued seeds 64
-// at a time against the thresholds of that moment. Per-block bests live in LDS as 64-bit keys
-// (error bits, seed in the low 24 bits) updated with atomic minimum, so the
-// result does not depend on the order in which survivors are evaluated; ties
-// within 2^-28 relative go to the smaller seed. A pilot pass over the first
-// seed tile finds, per lane, the seed with the smallest bound; their exact
-// errors start every block's best, so that the walk does not begin with an
-// infinite threshold. The final codes go through the same queue.
+// (seedq_exact.h). At P <= 3 a lane whose fold passes first stores its 16
+// bounds as a record; records are turned into queued seeds 64 at a time
+// against the thresholds of that moment. Every block's best is its exact fp64
+// error (an atomic minimum on the bit pattern in LDS) and the smallest seed of
+// that error (record_best), so the result is the exhaustive search's, ties to
+// the smallest seed, whatever the order in which survivors are evaluated. A
+// pilot pass over the first seed tile finds, per lane, the seed with the
+// smallest bound; their exact errors start every block's best, so that the
+// walk does not begin with an infinite threshold. The final codes go through
+// the same queue.
 //
 // Work split. A workgroup is 4 independent waves; a wave owns 4 tiles of 32
 // blocks (128 blocks) and walks the seed tiles once, reusing each A fragment
 // for its 4 block tiles; its B fragments stay in registers for the whole walk.
-// Large rungs walk the seed tiles in sequential chunks and small uniform
-// searches in concurrent ranges (see "seed ranges" below).
+// Large rungs walk the seed tiles in sequential chunks (see "seed chunks"
+// below).
 // Block tiles go to the matrix core in pairs (six products) before the vector
 // ALU folds them, with one branch per pair; the fold waits on its own
 // products, so it is occupancy (several waves per SIMD) that keeps the matrix
@@ -79,7 +80,7 @@ constexpr int kRecCapR = kRecFlushR + 64;
 constexpr int kRecRound = 32;
 constexpr int kRecQueueWords = 64 + kRecRound * 16;
 static_assert(kRecQueueWords % 4 == 0, "records start 16-byte aligned");
-static_assert(kRecQueueWords + 17 * kRecCapR + 128 + 32 <= kQCapFiltered,
+static_assert(kRecQueueWords + 17 * kRecCapR + 128 + 64 <= kQCapFiltered,
               "the record stage fits the per-wave pool");
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
@@ -200,6 +201,49 @@ SEEDQ_INLINE uint32_t seed_of(uint32_t seedbase, int j, int h) {
   return seedbase + 8u * uint32_t(j / 4) + 4u * uint32_t(h) + uint32_t(j % 4);
 }
 
+// Per-block best of a search: the exact fp64 error of the best code so far,
+// as its bit pattern (errors are >= 0, so the bits order like the values), in
+// LDS, and its seed, the smallest among the codes of exactly that error, in the
+// caller's seed array (12 more bytes of LDS per block cost a workgroup per CU:
+// measured 11 % slower at (16,3)). A block is only ever touched by the one wave
+// that owns it, so one evaluation batch (a candidate per lane, `mine`) updates
+// both in four steps: every lane lowers the error; if any lane tied or
+// improved, every lane reads the minimum the batch left; a lane that holds
+// that minimum while its block held a larger one before resets the seed with
+// an atomic exchange that the wave waits for (vmcnt(0): performed in L2; no
+// device-wide fence, which on this GPU writes back and invalidates the L2);
+// then every lane that holds the minimum lowers the seed to its own. Ties in
+// the exact error go to the smallest seed, and the result does not depend on
+// the order in which candidates are evaluated.
+SEEDQ_INLINE void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+SEEDQ_INLINE void record_best(unsigned long long* best, uint32_t* seed_best, int slot, int64_t b,
+                              double err, uint32_t seed, bool mine) {
+  const unsigned long long eb = mine ? (unsigned long long)__double_as_longlong(err) : 0ull;
+  unsigned long long old = 0ull;
+  if (mine) old = atomicMin(&best[slot], eb);
+  const bool cand = mine && eb <= old;
+  if (__builtin_amdgcn_ballot_w64(cand) == 0ull) return;
+  __threadfence_block();
+  const unsigned long long now = cand ? best[slot] : ~0ull;
+  const bool holds = cand && eb == now;
+  const bool reset = holds && old != now;
+  if (__builtin_amdgcn_ballot_w64(reset) != 0ull) {
+    if (reset) {
+      const uint32_t prev = __hip_atomic_exchange(&seed_best[b], seed, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+      asm volatile("" ::"v"(prev));   // keep the returning form
+    }
+    wait_vmem();
+  }
+  if (holds) __hip_atomic_fetch_min(&seed_best[b], seed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The best seed of block b once the wave's updates are performed.
+SEEDQ_INLINE uint32_t best_seed(const uint32_t* seed_best, int64_t b) {
+  return __hip_atomic_load(&seed_best[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Number of lanes below this one whose bit is set in mask.
 SEEDQ_INLINE int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0u));
@@ -211,19 +255,6 @@ SEEDQ_INLINE uint32_t lane_now() {
   uint32_t l;
   asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
   return l;
-}
-
-// Concurrent seed ranges of a launch: nconc_arg > 0 is the number itself;
-// nconc_arg < 0 lets the launch choose, from its rung's block count, enough
-// ranges for two waves per wave slot (1024 SIMDs at waves_per_simd), at most
-// -nconc_arg. Wave-uniform; count >= 1.
-__device__ __forceinline__ int concurrent_ranges(int nconc_arg, int64_t count, int waves_per_simd) {
-  if (nconc_arg > 0) return nconc_arg;
-  const int64_t waves = (count + kSlots - 1) / kSlots;
-  const int64_t want = 2 * 1024 * int64_t(waves_per_simd);
-  if (waves >= want) return 1;
-  const int64_t n = (want + waves - 1) / waves;
-  return int(n < -nconc_arg ? n : -nconc_arg);
 }
 
 // Queue entries: seed << 8 | final << 7 | slot (slot < 128). Seed 0 = no-op.
@@ -248,12 +279,14 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                   float* __restrict__ err_out, int nchunks, int chunk, int nconc_arg,
-                   unsigned long long* __restrict__ split_keys) {
-  __shared__ unsigned long long keys_all[kWaves][kSlots];
+                   float* __restrict__ err_out, int nchunks, int chunk,
+                   unsigned long long* __restrict__ carry) {
+  __shared__ unsigned long long best_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
   __shared__ float thr_base_all[kWaves][kSlots];   // ||w||^2 (1 - gamma) in accumulator units
-  __shared__ int8_t ex_all[kWaves][kSlots];        // power-of-two scaling of the block
+  // power-of-two scaling of the block: ilogb of its largest |w_i|, down to -149
+  // for fp32 subnormals, so 16 bits
+  __shared__ int16_t ex_all[kWaves][kSlots];
   __shared__ float4 rec_all[kWaves][kRecCap][4];   // 16 bounds per record
   __shared__ uint32_t meta_all[kWaves][kRecCap];
   __shared__ uint32_t queue_all[kWaves][kQCapRec];
@@ -263,10 +296,10 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int n = lane & 31;   // block column of the MFMA tile
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
-  unsigned long long* keys = keys_all[wave];
+  unsigned long long* best = best_all[wave];
   int32_t* blk = blk_all[wave];
   float* slot_thr = thr_base_all[wave];
-  int8_t* slot_ex = ex_all[wave];
+  int16_t* slot_ex = ex_all[wave];
   float4 (*rec)[4] = rec_all[wave];
   uint32_t* meta = meta_all[wave];
   uint32_t* queue = queue_all[wave];
@@ -278,8 +311,6 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   }
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
-  const int nconc = concurrent_ranges(nconc_arg, count, 3);
-  if (int(blockIdx.y) >= nconc) return;  // a range this rung does not need
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
 
   // ---------------------------------------------------------------- prologue
@@ -309,23 +340,26 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     bop[nt][1] = b_fragment<1>(ws, h);
     bop[nt][2] = b_fragment<2>(ws, h);
     if (h == 0) {
-      // a later launch of a sequential range split starts from the best so far
-      keys[nt * 32 + n] = chunk > 0 && valid[nt] ? split_keys[b] : ~0ull;
+      // a later chunk starts from the best so far (error in carry, seed in
+      // seed_out); the first one from none
+      best[nt * 32 + n] = chunk > 0 && valid[nt] ? carry[b] : ~0ull;
+      if (chunk == 0 && valid[nt]) seed_out[b] = ~0u;
       blk[nt * 32 + n] = int32_t(b);
       // thresholds live in accumulator units (both operands carry 2^12)
       slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
-      slot_ex[nt * 32 + n] = int8_t(ex);
+      slot_ex[nt * 32 + n] = int16_t(ex);
     }
   }
   __threadfence_block();
+  wait_vmem();   // the seed resets are performed before any update of them
 
-  // Screening threshold of slot s from its key: a bound passes when it can
+  // Screening threshold of slot s from its best: a bound passes when it can
   // reach the block's best exact error so far (-inf before the first one).
   auto slot_threshold = [&](int s) __attribute__((always_inline)) {
-    const unsigned long long key = keys[s];
+    const unsigned long long key = best[s];
     if (key == ~0ull) return -INFINITY;
-    const double bound = key_error(key) * (1.0 + 0x1p-27);
-    return slot_thr[s] - __double2float_ru(ldexp(bound, 24 - 2 * int(slot_ex[s])));
+    return slot_thr[s] - __double2float_ru(ldexp(__longlong_as_double((long long)key),
+                                                 24 - 2 * int(slot_ex[s])));
   };
   auto refresh = [&]() __attribute__((always_inline)) {
     __threadfence_block();
@@ -342,17 +376,21 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     while (qcount >= min_batch && qcount > 0) {
       const int e = qcount < 64 ? qcount : 64;
       const int base = qcount - e;
+      bool mine = false;
+      uint32_t seed = 0u;
+      int slot = 0;
+      int64_t b = 0;
+      double err = 0.0;
       if (lane < e) {
         const uint32_t ent = queue[base + lane];
-        const uint32_t seed = ent >> 8;
-        const int slot = int(ent & 0x7Fu);
+        seed = ent >> 8;
+        slot = int(ent & 0x7Fu);
         if (seed != 0u) {
-          const int64_t b = blk[slot];
+          b = blk[slot];
           float w[kC];
           load_block(W, b, true, w);
           int qe, q[P];
-          const double err =
-              exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
           if (ent & kFinal) {
             seed_out[b] = seed;
             exp_out[b] = uint8_t(qe);
@@ -366,10 +404,11 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
             reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
             if (err_out) err_out[b] = float(err);
           } else {
-            atomicMin(&keys[slot], (unsigned long long)candidate_key(err, seed));
+            mine = true;
           }
         }
       }
+      record_best(best, seed_out, slot, b, err, seed, mine);
       qcount = base;
     }
     __threadfence_block();
@@ -425,8 +464,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // ---------------------------------------------------------------- pilot
   // Over the first tile each lane tracks its seed of smallest bound; their
   // exact errors start every block's best. (Longer pilots cost more matrix
-  // time than the survivors they save.) Later launches of a sequential range
-  // split start from the keys instead.
+  // time than the survivors they save.) Later chunks start from the best so far
+  // instead.
   if (chunk > 0) {
     refresh();
   } else {
@@ -499,10 +538,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // loaded while the other tile is screened. The loads are unconditional (the
   // index is clamped to the last tile) so that the wait before each tile
   // covers only that tile's own loads.
-  // Range blockIdx.y of chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
-  const int64_t C0 = int64_t(chunk) * ntiles / nchunks, C1 = int64_t(chunk + 1) * ntiles / nchunks;
-  const int64_t T0 = C0 + int64_t(blockIdx.y) * (C1 - C0) / nconc;
-  const int64_t T1 = C0 + int64_t(blockIdx.y + 1) * (C1 - C0) / nconc;
+  // Chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
+  const int64_t T0 = int64_t(chunk) * ntiles / nchunks, T1 = int64_t(chunk + 1) * ntiles / nchunks;
   const int64_t last = T1 - 1;
   half8 x0 = A[T0 * 192 + lane], x1 = A[T0 * 192 + 64 + lane], x2 = A[T0 * 192 + 128 + lane];
   half8 y0, y1, y2;
@@ -526,23 +563,23 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   evaluate(1);
 
   // ---------------------------------------------------------------- results
-  // A seed split only folds its best keys into the global ones; the codes are
-  // emitted once all splits are done.
-  if (split_keys) {
+  // A chunk before the last hands its best errors on to the next launch (the
+  // seeds are in seed_out already); the last one emits the codes.
+  if (chunk + 1 < nchunks) {
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt)
-      if (h == 0 && active[nt]) atomicMin(&split_keys[blk[nt * 32 + n]], keys[nt * 32 + n]);
+      if (h == 0 && valid[nt]) carry[blk[nt * 32 + n]] = best[nt * 32 + n];
     return;
   }
+  wait_vmem();   // every seed update of this wave is performed
   // the winning seed of every block, evaluated once more to emit its code
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
     const bool put = h == 0 && active[nt];
     const uint64_t mk = ballot(put);
     if (put) {
-      const unsigned long long key = keys[nt * 32 + n];
-      // every active block has a key after the pilot; seed 1 is a guard
-      const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
+      // every active block has a best after the pilot; seed 1 is a guard
+      const uint32_t seed = best[nt * 32 + n] == ~0ull ? 1u : best_seed(seed_out, blk[nt * 32 + n]);
       queue[qcount + lanes_below(mk)] = (seed << 8) | kFinal | uint32_t(nt * 32 + n);
     }
     qcount += __popcll(mk);
@@ -571,12 +608,12 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
                    const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
                    int8_t* __restrict__ q_out, float* __restrict__ err_out, int nchunks,
-                   int chunk, int nconc_arg, unsigned long long* __restrict__ split_keys) {
+                   int chunk, unsigned long long* __restrict__ carry) {
   // With the record stage (kRec, P = 4 only) the per-wave pool holds the
   // candidate queue, the records (16 bounds and a meta word each) and the
   // per-slot threshold data; otherwise it is the queue alone.
   static_assert(!kRec || P == kRecordP, "records only at P = 4");
-  __shared__ unsigned long long keys_all[kWaves][kSlots];
+  __shared__ unsigned long long best_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
   __shared__ __attribute__((aligned(16))) uint32_t pool_all[kWaves][kQCapFiltered];
 
@@ -586,14 +623,14 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   const int wave = kRec ? __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6)) : int(threadIdx.x >> 6);
   const int n = lane & 31;   // block column of the MFMA tile
   const int h = lane >> 5;   // which half of the rows / reduction this lane holds
-  unsigned long long* keys = keys_all[wave];
+  unsigned long long* best = best_all[wave];
   int32_t* blk = blk_all[wave];
   uint32_t* pool = pool_all[wave];
   uint32_t* queue = pool;
   float4 (*rec)[4] = reinterpret_cast<float4 (*)[4]>(pool + kRecQueueWords);
   uint32_t* meta = pool + kRecQueueWords + 16 * kRecCapR;
   float* slot_thr = reinterpret_cast<float*>(meta + kRecCapR);
-  int8_t* slot_ex = reinterpret_cast<int8_t*>(slot_thr + kSlots);
+  int16_t* slot_ex = reinterpret_cast<int16_t*>(slot_thr + kSlots);   // ilogb, down to -149
 
   int64_t begin = 0, count = nblocks;
   if (list) {
@@ -602,8 +639,6 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   }
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
-  const int nconc = concurrent_ranges(nconc_arg, count, 4);
-  if (int(blockIdx.y) >= nconc) return;  // a range this rung does not need
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
 
   // ---------------------------------------------------------------- prologue
@@ -612,8 +647,10 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     const int64_t idx = wave_base + nt * 32 + n;
     const int64_t b = idx < count ? (list ? int64_t(list[begin + idx]) : idx) : 0;
     if (h == 0) {
-      // a later launch of a sequential range split starts from the best so far
-      keys[nt * 32 + n] = chunk > 0 && idx < count ? split_keys[b] : ~0ull;
+      // a later chunk starts from the best so far (its seed is already in
+      // seed_out); the first one from none
+      best[nt * 32 + n] = chunk > 0 && idx < count ? carry[b] : ~0ull;
+      if (chunk == 0 && idx < count) seed_out[b] = ~0u;
       blk[nt * 32 + n] = int32_t(b);
     }
     if constexpr (kRec) {
@@ -632,11 +669,12 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
           ww = fmaf(ws, ws, ww);
         }
         slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
-        slot_ex[nt * 32 + n] = int8_t(ex);
+        slot_ex[nt * 32 + n] = int16_t(ex);
       }
     }
   }
   __threadfence_block();
+  wait_vmem();   // the seed resets are performed before any update of them
 
   // Per-lane block data: the B fragments (2^12-scaled pair products of the
   // block scaled by a power of two so that max |w_i| lies in [1, 2)) and the
@@ -665,12 +703,12 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       bop[nt][1] = b_fragment<1>(ws, h);
       bop[nt][2] = b_fragment<2>(ws, h);
       // -inf before a block's first exact error, +inf for blocks not searched
-      const unsigned long long key = keys[nt * 32 + n];
+      const unsigned long long key = best[nt * 32 + n];
       const float thr_base = ww * one_minus_gamma * (kOperandScale * kOperandScale);
-      const double bound = key_error(key) * (1.0 + 0x1p-27);
       thr[nt] = !active ? INFINITY
                 : key == ~0ull ? -INFINITY
-                : thr_base - __double2float_ru(ldexp(bound, 24 - 2 * ex));
+                : thr_base - __double2float_ru(ldexp(__longlong_as_double((long long)key),
+                                                     24 - 2 * ex));
     }
   };
 
@@ -697,7 +735,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
         ent = queue[i + lane];
         const uint32_t seed = ent >> 8;
         const int slot = int(ent & 0x7Fu);
-        const unsigned long long key = keys[slot];
+        const unsigned long long key = best[slot];
         keep = seed != 0u;
         if (keep && !(ent & kFinal) && key != ~0ull) {
           float w[kC];
@@ -727,8 +765,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
             c = fmaf(b.w, ws[7], c);
             ss = fmaf(c, c, ss);
           }
-          const double bound = key_error(key) * (1.0 + 0x1p-27);
-          const float bu = __double2float_ru(ldexp(bound, -2 * ex)) * (1.0f + 0x1p-20f);
+          const float bu = __double2float_ru(ldexp(__longlong_as_double((long long)key), -2 * ex)) *
+                           (1.0f + 0x1p-20f);
           keep = ss >= ww * (1.0f - 0x1p-16f) - bu;
         }
       }
@@ -747,17 +785,21 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     while (nf >= min_batch && nf > 0) {
       const int e = nf < 64 ? nf : 64;
       const int base = nf - e;
+      bool mine = false;
+      uint32_t seed = 0u;
+      int slot = 0;
+      int64_t b = 0;
+      double err = 0.0;
       if (lane < e) {
         const uint32_t ent = queue[base + lane];
-        const uint32_t seed = ent >> 8;
-        const int slot = int(ent & 0x7Fu);
+        seed = ent >> 8;
+        slot = int(ent & 0x7Fu);
         if (seed != 0u) {
-          const int64_t b = blk[slot];
+          b = blk[slot];
           float w[kC];
           load_block(W, b, true, w);
           int qe, q[P];
-          const double err =
-              exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
           if (ent & kFinal) {
             seed_out[b] = seed;
             exp_out[b] = uint8_t(qe);
@@ -771,10 +813,11 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
             reinterpret_cast<uint2*>(q_out)[b] = make_uint2(lo, hi);
             if (err_out) err_out[b] = float(err);
           } else {
-            atomicMin(&keys[slot], (unsigned long long)candidate_key(err, seed));
+            mine = true;
           }
         }
       }
+      record_best(best, seed_out, slot, b, err, seed, mine);
       nf = base;
       ran = true;
     }
@@ -805,12 +848,11 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       if (lane < e) {
         m = meta[base + lane];
         const int sl = int(m & 0x7Fu);
-        const unsigned long long key = keys[sl];
+        const unsigned long long key = best[sl];
         t = -INFINITY;
-        if (key != ~0ull) {
-          const double bound = key_error(key) * (1.0 + 0x1p-27);
-          t = slot_thr[sl] - __double2float_ru(ldexp(bound, 24 - 2 * int(slot_ex[sl])));
-        }
+        if (key != ~0ull)
+          t = slot_thr[sl] - __double2float_ru(ldexp(__longlong_as_double((long long)key),
+                                                     24 - 2 * int(slot_ex[sl])));
         r0 = rec[base + lane][0];
         r1 = rec[base + lane][1];
         r2 = rec[base + lane][2];
@@ -867,8 +909,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // ---------------------------------------------------------------- pilot
   // Over the first tile each lane takes its seed of smallest bound; their exact
   // errors start every block's best. (Longer pilots cost more matrix time than
-  // the survivors they save.) Later launches of a sequential range split start
-  // from the keys (setup() above has turned them into thresholds).
+  // the survivors they save.) Later chunks start from the best so far (setup()
+  // above has turned it into thresholds).
   if (chunk == 0) {
     const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
 #pragma unroll
@@ -941,10 +983,8 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
 
   // Seed-tile fragments; the index is clamped to the last tile so that every
   // load is unconditional and each wait covers only the tile it is for.
-  // Range blockIdx.y of chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
-  const int64_t C0 = int64_t(chunk) * ntiles / nchunks, C1 = int64_t(chunk + 1) * ntiles / nchunks;
-  const int64_t T0 = C0 + int64_t(blockIdx.y) * (C1 - C0) / nconc;
-  const int64_t T1 = C0 + int64_t(blockIdx.y + 1) * (C1 - C0) / nconc;
+  // Chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
+  const int64_t T0 = int64_t(chunk) * ntiles / nchunks, T1 = int64_t(chunk + 1) * ntiles / nchunks;
   const int64_t last = T1 - 1;
   auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
     const half8* At = A + (T < last ? T : last) * 192;
@@ -1031,28 +1071,27 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   flush(1);
 
   // ---------------------------------------------------------------- results
-  // A seed split only folds its best keys into the global ones.
-  if (split_keys) {
+  // A chunk before the last hands its best errors on to the next launch (the
+  // seeds are in seed_out already); the last one emits the codes.
+  if (chunk + 1 < nchunks) {
 #pragma unroll
-    for (int nt = 0; nt < kNB; ++nt) {
-      const unsigned long long key = keys[nt * 32 + n];
-      if (h == 0 && wave_base + nt * 32 + n < count && key != ~0ull)
-        atomicMin(&split_keys[blk[nt * 32 + n]], key);
-    }
+    for (int nt = 0; nt < kNB; ++nt)
+      if (h == 0 && wave_base + nt * 32 + n < count) carry[blk[nt * 32 + n]] = best[nt * 32 + n];
     return;
   }
+  wait_vmem();   // every seed update of this wave is performed
   // The winning seed of every block, evaluated once more to emit its code.
-  // Every searched block holds a key after the pilot; a valid block without
+  // Every searched block holds a best after the pilot; a valid block without
   // one is all zero, where every seed ties and the smallest wins.
 #pragma unroll
   for (int nt = 0; nt < kNB; ++nt) {
     const bool valid = wave_base + nt * 32 + n < count;
-    const unsigned long long key = keys[nt * 32 + n];
+    const unsigned long long key = best[nt * 32 + n];
     const bool put = h == 0 && valid && key != ~0ull;
     const uint64_t mk = ballot(put);
     if (put)
       queue[qcount + lanes_below(mk)] =
-          (uint32_t(key & 0xFFFFFFull) << 8) | kFinal | uint32_t(nt * 32 + n);
+          (best_seed(seed_out, blk[nt * 32 + n]) << 8) | kFinal | uint32_t(nt * 32 + n);
     qcount += __popcll(mk);
     if (h == 0 && valid && key == ~0ull) {
       const int64_t b = blk[nt * 32 + n];
@@ -1065,82 +1104,17 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   flush(1);
 }
 
-// ---------------------------------------------------------------- seed ranges
-// The seed tiles of a rung can be walked in several ranges: in sequence, one
-// launch per chunk of kChunkTiles tiles, so that every wave walks the same 6 MB
-// of projector fragments at about the same time and they stay in L2 (one walk
-// over a 101 MB stack at K = 20 missed L2 on most requests); and, for a
-// search too small to fill the GPU, several ranges at once (grid dimension y;
-// a multi-rung call's launch trims them to its rung's block count on the
-// GPU). The per-block keys of all ranges meet in a global minimum held
-// in the caller's mantissa output (8 bytes per block, 8-byte aligned); a later
-// launch starts from it, so the thresholds carry over and only the first one
-// runs the pilot. Keys order candidates by (error to 2^-28, seed) and every
-// range evaluates whatever could still win within it, so the final minimum is
-// the key the unsplit search ends with. A last pass emits each block's code.
+// ---------------------------------------------------------------- seed chunks
+// The seed tiles of a large rung are walked in sequential chunks, one launch
+// per chunk of kChunkTiles tiles, so that every wave walks the same 6 MB of
+// projector fragments at about the same time and they stay in L2 (one walk
+// over a 101 MB stack at K = 20 missed L2 on most requests). Each block stays
+// with the same wave position in every launch; a chunk before the last leaves
+// the block's best exact error in the caller's mantissa output (8 bytes per
+// block, 8-byte aligned) and its seed in the seed output, and the next launch
+// starts from them, so only the first runs the pilot and the thresholds are as
+// tight as in one walk. The last chunk emits the codes.
 constexpr int64_t kChunkTiles = 2048;
-constexpr int64_t kRungRanges = 4;   // most concurrent ranges of a multi-rung rung's launch
-
-__device__ __forceinline__ bool rung_block(const int32_t* list, const int32_t* off, int rung,
-                                           int64_t nblocks, int64_t i, int64_t& b) {
-  int64_t begin = 0, count = nblocks;
-  if (list) {
-    begin = off[rung];
-    count = int64_t(off[rung + 1]) - begin;
-  }
-  if (i >= count) return false;
-  b = list ? int64_t(list[begin + i]) : i;
-  return true;
-}
-
-__global__ void __launch_bounds__(256)
-split_init_kernel(unsigned long long* __restrict__ keys, int64_t nblocks,
-                  const int32_t* __restrict__ list, const int32_t* __restrict__ off, int rung) {
-  int64_t b;
-  if (rung_block(list, off, rung, nblocks, int64_t(blockIdx.x) * 256 + threadIdx.x, b))
-    keys[b] = ~0ull;
-}
-
-template <int P>
-__global__ void __launch_bounds__(256)
-split_emit_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
-                  const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
-                  const double* __restrict__ pinv64, uint32_t* __restrict__ seed_out,
-                  uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
-                  float* __restrict__ err_out) {
-  int64_t b;
-  if (!rung_block(list, off, rung, nblocks, int64_t(blockIdx.x) * 256 + threadIdx.x, b)) return;
-  float w[kC];
-  load_block(W, b, true, w);
-  float amax = 0.f;
-#pragma unroll
-  for (int i = 0; i < kC; ++i) amax = fmaxf(amax, fabsf(w[i]));
-  uint2* qw = reinterpret_cast<uint2*>(q_out);
-  if (amax == 0.f) {
-    // all-zero block: every seed ties, the smallest one wins
-    seed_out[b] = 1u;
-    exp_out[b] = 15;
-    qw[b] = make_uint2(0u, 0u);
-    if (err_out) err_out[b] = 0.f;
-    return;
-  }
-  const unsigned long long key = reinterpret_cast<const unsigned long long*>(q_out)[b];
-  // every searched block holds a key after the pilot; seed 1 is a guard
-  const uint32_t seed = key == ~0ull ? 1u : uint32_t(key & 0xFFFFFFull);
-  int qe, q[P];
-  const double err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
-  seed_out[b] = seed;
-  exp_out[b] = uint8_t(qe);
-  uint32_t lo = 0, hi = 0;
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    const uint32_t byte = uint32_t(uint8_t(int8_t(q[p])));
-    if (p < 4) lo |= byte << (8 * p);
-    else hi |= byte << (8 * (p - 4));
-  }
-  qw[b] = make_uint2(lo, hi);
-  if (err_out) err_out[b] = float(err);
-}
 
 int64_t env_int(const char* name, int64_t fallback) {
   if (const char* env = std::getenv(name)) {
@@ -1149,20 +1123,6 @@ int64_t env_int(const char* name, int64_t fallback) {
     if (end != env && v >= 0) return v;
   }
   return fallback;
-}
-
-// Number of concurrent ranges for a uniform-rung search of nblocks blocks over
-// ntiles tiles: enough waves for two per wave slot (1024 SIMDs at the kernel's
-// occupancy), at most 256 ranges and at least 8 seed tiles per range.
-// SEEDQ_SEED_SPLITS overrides the choice (clamped to the same limits).
-int seed_splits(int64_t nblocks, int64_t ntiles, int waves_per_simd) {
-  const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(256, ntiles / 8));
-  const int64_t forced = env_int("SEEDQ_SEED_SPLITS", 0);
-  if (forced >= 1) return int(std::min<int64_t>(forced, smax));
-  const int64_t waves = (nblocks + kSlots - 1) / kSlots;
-  const int64_t want = 2 * 1024 * int64_t(waves_per_simd);
-  if (waves >= want) return 1;
-  return int(std::min<int64_t>(smax, (want + waves - 1) / waves));
 }
 
 template <int P>
@@ -1192,32 +1152,12 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.q_out = d_q;
   a.err_out = d_err;
   // Sequential chunks of the seed tiles (SEEDQ_SEED_CHUNK_TILES overrides the
-  // chunk length; 0 = one chunk), then concurrent ranges within each chunk:
-  // for a uniform-rung search the number follows from its block count, known
-  // here; a rung of a multi-rung call learns its count on the GPU, so its
-  // launches get up to kRungRanges ranges that each launch trims to what the
-  // count needs (nconc_arg < 0).
+  // chunk length; 0 = one chunk; at least 8 tiles per chunk).
   const int64_t chunk_tiles = env_int("SEEDQ_SEED_CHUNK_TILES", kChunkTiles);
   const int64_t nseq =
       chunk_tiles > 0 ? std::max<int64_t>(1, std::min<int64_t>(L.ntiles / 8, L.ntiles / chunk_tiles)) : 1;
-  const int64_t per_chunk = L.ntiles / nseq;
-  const int occ = P >= 4 ? 4 : 3;
-  int nconc_arg = 1;
-  if (!d_list)
-    nconc_arg = seed_splits(nblocks, per_chunk, occ);
-  else if (env_int("SEEDQ_SEED_SPLITS", 0) >= 1)
-    nconc_arg = seed_splits(1, per_chunk, occ);   // the override, clamped
-  else if (per_chunk >= 16)
-    nconc_arg = -int(std::min<int64_t>(kRungRanges, per_chunk / 8));
-  const int grid_y = nconc_arg > 0 ? nconc_arg : -nconc_arg;
-  unsigned long long* keys = nullptr;
-  const unsigned nb256 = unsigned((nblocks + 255) / 256);
-  if (nseq > 1 || grid_y > 1) {
-    keys = reinterpret_cast<unsigned long long*>(d_q);
-    hipLaunchKernelGGL(split_init_kernel, dim3(nb256), dim3(256), 0, stream, keys, nblocks, a.list,
-                       a.off, a.rung);
-  }
-  const dim3 grid = dim3(unsigned(blocks), unsigned(grid_y), 1u);
+  unsigned long long* carry = reinterpret_cast<unsigned long long*>(d_q);
+  const dim3 grid = dim3(unsigned(blocks), 1u, 1u);
   for (int64_t c = 0; c < nseq; ++c) {
     if constexpr (P >= 4) {
       auto kern = search_mfma_remat_kernel<P, false>;
@@ -1227,18 +1167,14 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
                          stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
                          reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
                          a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, int(nseq),
-                         int(c), nconc_arg, keys);
+                         int(c), carry);
     } else {
       hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
                          a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
                          a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
-                         int(nseq), int(c), nconc_arg, keys);
+                         int(nseq), int(c), carry);
     }
   }
-  if (keys)
-    hipLaunchKernelGGL(split_emit_kernel<P>, dim3(nb256), dim3(256), 0, stream, a.W, nblocks,
-                       a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.seed_out, a.exp_out, a.q_out,
-                       a.err_out);
   return hipGetLastError();
 }
 

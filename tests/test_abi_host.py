@@ -31,7 +31,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(sq):
     names = _declared()
-    assert len(names) == 26
+    assert len(names) == 30
     L = ctypes.CDLL(sq.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
