@@ -59,6 +59,7 @@ extern "C" {
 #define SEEDQ_EHULL (-4)        /* damages missing, not finite, or no rung left on the hull */
 #define SEEDQ_EHIP (-5)         /* a HIP launch or copy failed */
 #define SEEDQ_EWORKSPACE (-6)   /* workspace missing or smaller than required */
+#define SEEDQ_ESCRATCH (-7)     /* larger than the fixed scratch of seedq_compress_noalloc */
 
 #define SEEDQ_BLOCK 8           /* C: weights per block (section 3.1, B = 8) */
 #define SEEDQ_MAX_RUNGS 8
@@ -208,6 +209,32 @@ int seedq_compress(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
                    const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
                    uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
                    void* d_workspace, size_t workspace_bytes, void* hip_stream);
+
+/*
+ * seedq_compress without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and errors as
+ * seedq_compress, from the same kernels; the scratch a multi-rung call needs
+ * (the per-rung block lists, seedq_compress_workspace_bytes of it) comes from a
+ * fixed device array of SEEDQ_NOALLOC_SCRATCH_BYTES (128 MiB) that each GPU the
+ * library runs on holds until the process ends. The call allocates nothing: no
+ * hipMalloc, no hipFree, no allocating library routine; the first call on a
+ * device looks up that device's array (hipGetSymbolAddress).
+ * A problem whose workspace would exceed the array (more than about 33.5 M
+ * blocks with several rungs) is rejected with SEEDQ_ESCRATCH before anything is
+ * enqueued; a single-rung call needs no scratch and has no such limit.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams or from different threads) race and must be ordered by
+ * the caller. Nothing in the array needs to start at zero; it keeps the last
+ * call's lists.
+ * Asynchronous on hip_stream. Errors: SEEDQ_EINVAL, SEEDQ_EUNSUPPORTED,
+ * SEEDQ_ESCRATCH, SEEDQ_EHIP.
+ */
+#define SEEDQ_NOALLOC_SCRATCH_BYTES (128u << 20)
+int seedq_compress_noalloc(const float* d_W, int64_t nrows, int64_t ncols, int32_t C,
+                           const uint8_t* d_rung_of_block, int32_t nrungs, const seedq_bases* bases,
+                           uint32_t* d_seed, uint8_t* d_exp, int8_t* d_q, float* d_err,
+                           void* hip_stream);
 
 /*
  * Reconstruction w_hat = U(s) q 2^-e for every block (Algorithm 2, the

@@ -87,6 +87,9 @@ def lib() -> ctypes.CDLL:
         L.seedq_compress.restype = ctypes.c_int
         L.seedq_compress.argtypes = [vp, i64, i64, i32, vp, i32, ctypes.POINTER(BasesRef), vp, vp,
                                      vp, vp, vp, sz, vp]
+        L.seedq_compress_noalloc.restype = ctypes.c_int
+        L.seedq_compress_noalloc.argtypes = [vp, i64, i64, i32, vp, i32, ctypes.POINTER(BasesRef),
+                                             vp, vp, vp, vp, vp]
         L.seedq_decompress.restype = ctypes.c_int
         L.seedq_decompress.argtypes = [vp, vp, vp, vp, i32, ctypes.POINTER(Rung), i64, i64, i32,
                                        vp, vp, vp]
@@ -211,6 +214,15 @@ def seedq_compress(d_W, nrows: int, ncols: int, C: int, d_rung_of_block, bases: 
                               _ptr(d_seed), _ptr(d_exp), _ptr(d_q), _ptr(d_err),
                               _ptr(d_workspace), workspace_bytes, _stream(stream))
     _check(rc, "seedq_compress")
+
+
+def seedq_compress_noalloc(d_W, nrows: int, ncols: int, C: int, d_rung_of_block, bases: list,
+                           d_seed, d_exp, d_q, d_err, stream=None) -> None:
+    arr = (BasesRef * len(bases))(*[BasesRef(b.K, b.P, _ptr(b.buffer)) for b in bases])
+    rc = lib().seedq_compress_noalloc(_ptr(d_W), nrows, ncols, C, _ptr(d_rung_of_block), len(bases),
+                                      arr, _ptr(d_seed), _ptr(d_exp), _ptr(d_q), _ptr(d_err),
+                                      _stream(stream))
+    _check(rc, "seedq_compress_noalloc")
 
 
 def seedq_decompress(d_seed, d_exp, d_q, d_rung_of_block, rungs, nrows: int, ncols: int, C: int,

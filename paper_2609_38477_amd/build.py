@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 HIP_SOURCES = ["seedq_bases.hip", "seedq_search_mfma.hip", "seedq_compact.hip",
                "seedq_decompress.hip", "seedq_stream.hip",
-               "seedq_footprint.hip", "seedq_frontend.hip"]
+               "seedq_footprint.hip", "seedq_frontend.hip", "seedq_noalloc.hip"]
 HOST_SOURCES = ["seedq_api.cpp", "seedq_schedule.cpp", "seedq_frontend_host.cpp"]
 
 # Device code is compiled without packed fp32 instructions.

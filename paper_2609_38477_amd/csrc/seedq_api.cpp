@@ -68,6 +68,8 @@ const char* seedq_strerror(int code) {
     case SEEDQ_EHULL: return "damages missing or no usable rung on the lower convex hull";
     case SEEDQ_EHIP: return "HIP launch failed";
     case SEEDQ_EWORKSPACE: return "workspace missing or too small";
+    case SEEDQ_ESCRATCH:
+      return "problem larger than the fixed scratch of the allocation-free compress call";
     default: return "unknown error";
   }
 }

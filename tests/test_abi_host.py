@@ -31,7 +31,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(sq):
     names = _declared()
-    assert len(names) == 30
+    assert len(names) == 31
     L = ctypes.CDLL(sq.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(sq):
 
 def test_strerror(sq):
     assert "success" in sq.seedq_strerror(0)
-    for c in range(-6, 0):
+    for c in range(-7, 0):
         assert sq.seedq_strerror(c) != sq.seedq_strerror(0)
 
 
@@ -72,6 +72,26 @@ def test_compress_argument_errors_need_no_gpu(sq):
     assert L.seedq_compress(256, 8, 8, 8, None, 1, b3, 256, 256, 256, None, None, 0, None) == -2
     assert sq.seedq_compress_workspace_bytes(4096, 4096, 8, 1) == 0
     assert sq.seedq_compress_workspace_bytes(4096, 4096, 8, 3) >= 4 * 4096 * 512
+
+
+def test_compress_noalloc_argument_errors_need_no_gpu(sq):
+    # the allocation-free call checks its arguments like seedq_compress, and a
+    # multi-rung problem whose block lists exceed its fixed 128 MiB scratch is
+    # rejected before anything touches a GPU
+    L = sq.lib()
+    b = (sq.BasesRef * 1)(sq.BasesRef(16, 3, 256))
+    assert L.seedq_compress_noalloc(None, 8, 8, 8, None, 1, b, 256, 256, 256, None, None) == -1
+    assert L.seedq_compress_noalloc(256, 8, 12, 8, None, 1, b, 256, 256, 256, None, None) == -1
+    assert L.seedq_compress_noalloc(256, 8, 8, 4, None, 1, b, 256, 256, 256, None, None) == -2
+    b2 = (sq.BasesRef * 2)(sq.BasesRef(12, 2, 256), sq.BasesRef(16, 3, 256))
+    assert L.seedq_compress_noalloc(256, 8, 8, 8, None, 2, b2, 256, 256, 256, None, None) == -1
+    # 4 bytes of list per block: 2^25 blocks need more than 128 MiB with the
+    # per-chunk counts; 2^25 - 2^20 blocks fit
+    assert sq.seedq_compress_workspace_bytes(1 << 14, 8 * (1 << 11), 8, 2) > 128 << 20
+    assert L.seedq_compress_noalloc(256, 1 << 14, 8 * (1 << 11), 8, 256, 2, b2, 256, 256, 256,
+                                    None, None) == -7
+    assert sq.seedq_compress_workspace_bytes(31 << 10, 8 * (1 << 10), 8, 8) <= 128 << 20
+    assert "scratch" in sq.seedq_strerror(-7)
 
 
 def _compare(sq, oq, nrows, ncols, rungs, damage, target, a, rho=None, f=0.06):
