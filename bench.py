@@ -364,6 +364,57 @@ def frontend_bench(args) -> int:
     return 0
 
 
+def row_tiles_bench(args) -> int:
+    """A layer streamed through the GPU in row tiles from pinned host memory
+    (two tiles resident at a time, the copy of the next tile overlapping the
+    search of this one) against one call on the whole resident matrix: the same
+    rungs, bases and search, codes compared bit for bit. Times are wall clock
+    between synchronisations; the streamed time includes its host-to-device
+    copies."""
+    import torch
+
+    import paper_2609_38477_amd as sq
+    import synthetic
+
+    wl = synthetic.WORKLOADS[args.workload]
+    log(f"row tiles on {wl.name}: {wl.note}")
+    W = synthetic.workload_weights(wl)
+    a = synthetic.importance_profile(wl.ncols)
+    rob, rep = sq.plan_schedule(wl.nrows, wl.ncols, wl.rungs, wl.damage, wl.target_bpw, a)
+    d_rob = torch.from_numpy(rob).cuda() if len(wl.rungs) > 1 else None
+    bases = [sq.build_bases(K, P) for K, P in wl.rungs]
+    W_host = torch.from_numpy(W).pin_memory()
+    cands = sum(int(rep["count"][r]) * ((1 << K) - 1) for r, (K, P) in enumerate(wl.rungs))
+
+    def run(fn):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out = fn()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, out
+
+    dW = torch.from_numpy(W).cuda()
+    run(lambda: sq.compress(dW, bases, rung_of_block=d_rob))            # warm-up
+    t_full, ref = run(lambda: sq.compress(dW, bases, rung_of_block=d_rob))
+    ref = [t.cpu() for t in ref]
+    del dW
+    torch.cuda.empty_cache()
+    out = {"metric": "row-tiled search against one resident call; 1 GPU", "workload": wl.name,
+           "shape": [wl.nrows, wl.ncols], "candidates": cands, "resident_s": t_full,
+           "resident_candidates_per_s": cands / t_full, "tiles": {}}
+    for tiles in args.row_tiles_list:
+        t, got = run(lambda: sq.compress_row_tiles(W_host, bases, rung_of_block=d_rob,
+                                                   row_tiles=tiles))
+        same = all(torch.equal(x.cpu(), y) for x, y in zip(got, ref))
+        out["tiles"][str(tiles)] = {"s": t, "over_resident": t / t_full, "identical_codes": same,
+                                    "resident_tile_bytes": 2 * 4 * wl.ncols * (-(-wl.nrows // tiles))}
+        log(f"{tiles} tiles: {t:.3f} s ({t / t_full:.3f} of resident), identical {same}")
+        del got
+    out["data"] = "synthetic"
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,6 +432,9 @@ def main() -> int:
                     help="time the importance front end on a 7B-shaped layer with the oracle beside it")
     ap.add_argument("--decoder", action="store_true",
                     help="time the decoder path (derive, pack, parse, decode, decode-GEMV) instead")
+    ap.add_argument("--row-tiles", type=str, default=None,
+                    help="comma-separated tile counts: time the search streamed in row tiles "
+                         "from host memory against one resident call (e.g. 2,4,8)")
     ap.add_argument("--gemm-reference-only", action="store_true",
                     help="only time the fp16 GEMM used as the practical matrix-core reference")
     args = ap.parse_args()
@@ -408,6 +462,9 @@ def main() -> int:
         return grid_bench(args)
     if args.frontend:
         return frontend_bench(args)
+    if args.row_tiles:
+        args.row_tiles_list = [int(t) for t in args.row_tiles.split(",")]
+        return row_tiles_bench(args)
     torch.cuda.set_device(torch.device("cuda:0"))
     wl = synthetic.WORKLOADS[args.workload]
     out, W = run_steps(wl, args.steps, args.warmup)

@@ -479,6 +479,64 @@ def compress(W, bases: list, rung_of_block=None, with_err: bool = True, stream=N
     return seed, exp, q, err
 
 
+def compress_row_tiles(W_host, bases: list, rung_of_block=None, row_tiles: int = 8,
+                       with_err: bool = True):
+    """Seed search of a matrix that stays in host memory, streamed through the
+    GPU in ``row_tiles`` contiguous row ranges (blocks are independent once the
+    rungs are planned, so every tile is one seedq_compress call on its rows and
+    their slice of the rung array). W_host: torch fp32 [nrows, ncols] on the
+    host, pinned for asynchronous copies. Two tile buffers alternate: the copy
+    of the next tile (on a copy stream) overlaps the search of this one (on the
+    current stream). Outputs as ``compress`` (device tensors); only two tiles of
+    W are ever resident in device memory."""
+    import torch
+    nrows, ncols = W_host.shape
+    G = ncols // SEEDQ_BLOCK
+    nb = nrows * G
+    dev = torch.device("cuda", torch.cuda.current_device())
+    seed = torch.empty(nb, dtype=torch.int32, device=dev)
+    exp = torch.empty(nb, dtype=torch.uint8, device=dev)
+    q = torch.empty((nb, SEEDQ_QSTRIDE), dtype=torch.int8, device=dev)
+    err = torch.empty(nb, dtype=torch.float32, device=dev) if with_err else None
+    bounds = [nrows * t // row_tiles for t in range(row_tiles + 1)]
+    rows_max = max(bounds[t + 1] - bounds[t] for t in range(row_tiles))
+    bufs = [torch.empty((rows_max, ncols), dtype=torch.float32, device=dev) for _ in range(2)]
+    nws = seedq_compress_workspace_bytes(rows_max, ncols, SEEDQ_BLOCK, len(bases))
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev) if nws else None
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream(device=dev)
+    copied = [torch.cuda.Event() for _ in range(2)]
+    searched = [torch.cuda.Event() for _ in range(2)]
+    # the tile buffers come from the current stream's pool, whose pending work
+    # may still read the memory they reuse: copies start after that work
+    copy.wait_stream(compute)
+
+    def upload(t):
+        r0, r1 = bounds[t], bounds[t + 1]
+        k = t % 2
+        if t >= 2:
+            copy.wait_event(searched[k])     # the buffer's previous tile is done
+        with torch.cuda.stream(copy):
+            bufs[k][: r1 - r0].copy_(W_host[r0:r1], non_blocking=True)
+            copied[k].record(copy)
+
+    upload(0)
+    for t in range(row_tiles):
+        r0, r1 = bounds[t], bounds[t + 1]
+        if t + 1 < row_tiles:
+            upload(t + 1)
+        k = t % 2
+        compute.wait_event(copied[k])
+        if r1 > r0:
+            b0, b1 = r0 * G, r1 * G
+            seedq_compress(bufs[k][: r1 - r0], r1 - r0, ncols, SEEDQ_BLOCK,
+                           None if rung_of_block is None else rung_of_block[b0:b1], bases,
+                           seed[b0:b1], exp[b0:b1], q[b0:b1], None if err is None else err[b0:b1],
+                           ws, nws, compute)
+        searched[k].record(compute)
+    return seed, exp, q, err
+
+
 def decompress(seed, exp, q, rungs, nrows: int, ncols: int, rung_of_block=None,
                with_acc: bool = False, stream=None):
     import torch

@@ -6,12 +6,19 @@
 
 namespace seedq {
 
+typedef short seedq_short2 __attribute__((ext_vector_type(2)));
+
 // Quantised error of seed s for block w (fp64, exact reconstruction).
-// A: pinv(U(s)), P x 8 row-major (fp64).
-template <int P>
+// A:  pinv(U(s)), P x 8 row-major (fp64).
+// kTable: read the states from the table Ub, else step the LFSR (mask) from s.
+// Ub: the seed's integer basis from the basis stack (see BasesLayout): for
+//     K <= kPackedMaxK, (P+1)/2 x 8 words, word (j, i) = the centred states
+//     u[2j][i] (low half) and u[2j+1][i] (high half) as int16; above it, P x 8
+//     int32 words u[j][i]. u[j][i] = x_{8j+i} - 2^(K-1), x_0 = s.
+template <int P, bool kTable>
 __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double* __restrict__ A,
-                                             uint32_t s, int K, uint32_t mask, int& e_out,
-                                             int (&q)[P]) {
+                                             const uint32_t* __restrict__ Ub, uint32_t s, int K,
+                                             uint32_t mask, int& e_out, int (&q)[P]) {
 #pragma clang fp contract(off)
   double t[P];
   int e = 15;
@@ -19,7 +26,7 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
   for (int p = 0; p < P; ++p) {
     double acc = 0.0;
 #pragma unroll
-    for (int i = 0; i < kC; ++i) acc = acc + A[p * kC + i] * double(w[i]);
+    for (int i = 0; i < kC; ++i) acc = fma(A[p * kC + i], double(w[i]), acc);
     t[p] = acc;
     // The largest e in [0, 15] at which every rne(t_p 2^e) lies in [-8, 7], in
     // closed form, folded into the coefficient loop. A positive t = f 2^E
@@ -41,21 +48,58 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
     const double r = fmin(fmax(rint(ldexp(t[p], e)), -8.0), 7.0);
     q[p] = int(r);
   }
-  // x - 2^(K-1) lies in [-2^23, 2^23) for K <= 24, so each product is one
-  // signed 24-bit multiply-add.
-  const int32_t half = int32_t(1) << (K - 1);
+  // acc_i = sum_j u[j][i] q_j, exact in int32 (|u| < 2^23, |q| <= 8, P <= 6).
+  // From the table the basis address is made to depend on e, so that its loads
+  // are issued after the coefficient loads are consumed and the two sets of
+  // registers are not live at once.
   int32_t acc[kC];
+  if constexpr (!kTable) {
+    // the states by LFSR steps from the seed: fewer registers than the table
+    // (x - 2^(K-1) lies in [-2^23, 2^23) for K <= 24: one 24-bit multiply-add)
+    const int32_t half = int32_t(1) << (K - 1);
 #pragma unroll
-  for (int i = 0; i < kC; ++i) acc[i] = 0;
-  uint32_t x = s;
+    for (int i = 0; i < kC; ++i) acc[i] = 0;
+    uint32_t x = s;
 #pragma unroll
-  for (int j = 0; j < P; ++j) {
+    for (int j = 0; j < P; ++j) {
 #pragma unroll
-    for (int i = 0; i < kC; ++i) {
-      acc[i] += __mul24(int32_t(x) - half, q[j]);
-      x = lfsr_step(x, mask);
+      for (int i = 0; i < kC; ++i) {
+        acc[i] += __mul24(int32_t(x) - half, q[j]);
+        x = lfsr_step(x, mask);
+      }
+    }
+  } else if (K <= kPackedMaxK) {
+    asm volatile("" : "+v"(Ub) : "v"(e));
+    // two coefficients per dot2 (v_dot2_i32_i16)
+    constexpr int PW = (P + 1) / 2;
+    const uint4* src = reinterpret_cast<const uint4*>(Ub);
+#pragma unroll
+    for (int i = 0; i < kC; ++i) acc[i] = 0;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const uint32_t qp = uint32_t(uint16_t(int16_t(q[2 * j]))) |
+                          (2 * j + 1 < P ? uint32_t(uint16_t(int16_t(q[2 * j + 1]))) << 16 : 0u);
+      const seedq_short2 qv = __builtin_bit_cast(seedq_short2, qp);
+      const uint4 lo = src[2 * j], hi = src[2 * j + 1];
+      const uint32_t u[kC] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+      for (int i = 0; i < kC; ++i)
+        acc[i] = __builtin_amdgcn_sdot2(__builtin_bit_cast(seedq_short2, u[i]), qv, acc[i], false);
+    }
+  } else {
+    asm volatile("" : "+v"(Ub) : "v"(e));
+    const uint4* src = reinterpret_cast<const uint4*>(Ub);
+#pragma unroll
+    for (int i = 0; i < kC; ++i) acc[i] = 0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const uint4 lo = src[2 * j], hi = src[2 * j + 1];
+      const uint32_t u[kC] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+      for (int i = 0; i < kC; ++i) acc[i] += __mul24(int32_t(u[i]), q[j]);
     }
   }
+  // the definition's error: index order, no fused multiply-add
   const int sh = -(K - 1 + e);
   double err = 0.0;
 #pragma unroll

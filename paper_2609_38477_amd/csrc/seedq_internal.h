@@ -54,18 +54,40 @@ constexpr int kTileBytes = kPairsPadded * kSeedTile * 2;   // 3 KB per seed tile
 // Pair index k of (i, j), i <= j, row-major over the upper triangle.
 __host__ __device__ constexpr int pair_index(int i, int j) { return i * kC - i * (i - 1) / 2 + (j - i); }
 
+// Rungs whose screen projects blocks onto an orthonormal basis of the
+// complement of range(U(s)) (8 - P vectors per seed) instead of forming the
+// quadratic form w^T Pi_s w: for large P that complement is small, and its
+// projection gives the least-squares residual without cancellation.
+constexpr int kComplementMinP = 5;
+__host__ __device__ constexpr int complement_dims(int P) { return P >= kComplementMinP ? kC - P : 0; }
+constexpr float kComplementScale = 256.0f;      // 2^8 on the complement operand
+
 // Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
 //   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
-//   q32:    float  [S][P][8]   orthonormal basis of range(U(s)) (rows of Q^T);
-//                               rows beyond the rank are zero (the fp32
-//                               residual filter of the P = 6 search reads it)
+//   ub:     uint32 [S][W] the integer basis u[j][i] = x_{8j+i} - 2^(K-1) of
+//           every seed (x_0 = s), W = basis_words(K, P) words: for K <=
+//           kPackedMaxK pairs of int16 (word j*8 + i = u[2j][i] | u[2j+1][i]
+//           << 16, zero high half past P), above it int32 (word j*8 + i =
+//           u[j][i]); the exact evaluation reads it instead of stepping the
+//           LFSR
 //   pi16:   fp16 [ntiles][3][64][8]  2^12 Pi_s[k] as MFMA A-operand fragments:
 //           tile T holds seeds 32T+1 .. 32T+32; fragment t, lane l, element e
 //           is pair k = 16t + 8(l/32) + e of seed 32T + (l%32) + 1 (zero for
 //           k >= 36 and for seeds beyond 2^K - 1)
+//   nc16:   fp16 [ntiles][M][64][8], M = complement_dims(P) (empty below
+//           kComplementMinP): MFMA A fragments of the complement basis n_c of
+//           range(U(s)), c < M; fragment c of tile T, lane l, element e is
+//           hi(2^8 n_c[e]) for l < 32 and lo(2^8 n_c[e]) = fp16(2^8 n_c[e] -
+//           hi) for l >= 32, of seed 32T + (l % 32) + 1 (zero beyond 2^K - 1)
+// Widest LFSR whose centred states fit int16 (|x - 2^(K-1)| <= 2^(K-1)).
+constexpr int kPackedMaxK = 16;
+__host__ __device__ constexpr int basis_words(int K, int P) {
+  return K <= kPackedMaxK ? kC * ((P + 1) / 2) : kC * P;
+}
+
 struct BasesLayout {
   int64_t nseeds, ntiles;
-  size_t off_pinv64, off_q32, off_pi16, total;
+  size_t off_pinv64, off_ub, off_pi16, off_nc16, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -75,9 +97,10 @@ inline BasesLayout bases_layout(int K, int P) {
   L.nseeds = (int64_t(1) << K) - 1;
   L.ntiles = (L.nseeds + kSeedTile - 1) / kSeedTile;
   L.off_pinv64 = 0;
-  L.off_q32 = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
-  L.off_pi16 = align256(L.off_q32 + size_t(L.nseeds) * P * kC * sizeof(float));
-  L.total = align256(L.off_pi16 + size_t(L.ntiles) * kTileBytes);
+  L.off_ub = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
+  L.off_pi16 = align256(L.off_ub + size_t(L.nseeds) * basis_words(K, P) * sizeof(uint32_t));
+  L.off_nc16 = align256(L.off_pi16 + size_t(L.ntiles) * kTileBytes);
+  L.total = align256(L.off_nc16 + size_t(L.ntiles) * complement_dims(P) * 64 * kC * 2);
   return L;
 }
 

@@ -12,12 +12,16 @@
 // accumulation. A candidate passes when its bound can be at most the block's
 // best error so far; the fp16 rounding of the operands is covered by the
 // margin gamma = sqrt(P) 2^-10 (1 + 2^-6) + 2^-14 (relative to ||w||^2), so no
-// candidate that could win is ever skipped.
+// candidate that could win is ever skipped. That margin is relative to
+// ||w||^2, while the bound itself is a difference: at P >= 5, where the best
+// errors are small beside ||w||^2, the screen instead computes r_LS directly as
+// the squared projections of w on 8 - P orthonormal vectors orthogonal to
+// range(U(s)) (complement_screen), whose rounding margin is relative to r_LS.
 //
 // Survivors. Each wave queues its passing (seed, block) pairs in LDS and
 // evaluates them 64 at a time, one per lane, with the exact fp64 evaluation
-// (seedq_exact.h). At P <= 3 a lane whose fold passes first stores its 16
-// bounds as a record; records are turned into queued seeds 64 at a time
+// (seedq_exact.h). In the first kernel a lane whose fold passes first stores
+// its 16 bounds as a record; records are turned into queued seeds 64 at a time
 // against the thresholds of that moment. Every block's best is its exact fp64
 // error (an atomic minimum on the bit pattern in LDS) and the smallest seed of
 // that error (record_best), so the result is the exhaustive search's, ties to
@@ -35,10 +39,12 @@
 // Block tiles go to the matrix core in pairs (six products) before the vector
 // ALU folds them, with one branch per pair; the fold waits on its own
 // products, so it is occupancy (several waves per SIMD) that keeps the matrix
-// core busy. For P >= 4 the fp64 evaluation needs more registers than the
-// walk leaves free, so a second kernel rebuilds the block data and reloads the
+// core busy. At P = 4 the fp64 evaluation needs more registers than the walk
+// leaves free, so a second kernel rebuilds the block data and reloads the
 // seed-tile fragments after every evaluation batch instead of keeping them
-// live across it, and runs at four waves per SIMD.
+// live across it, and runs at four waves per SIMD. (P >= 5 screens with the
+// complement projections below, whose block operand is a single fragment, and
+// stays in the first kernel.)
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
@@ -56,17 +62,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kWaves = 4;
 constexpr int kNB = 4;               // 32-block tiles per wave
 constexpr int kSlots = kNB * 32;     // blocks per wave
-// Queue entries per wave of the rebuilding kernel: with the residual filter up
-// to 63 filtered and 63 new entries wait before a pair of block tiles adds its
-// at most 2 x 1024.
-constexpr int kQCapFiltered = 128 + 2 * 1024;
-// Rungs that use the residual filter: it defers exact evaluations until 64
-// filtered entries wait, which pays only where most survivors of the matrix
-// core's screen fail the fp32 residual (measured on 2.1 M blocks: (16,6) and
-// (15,6) faster, (14,6) and below slower, P <= 5 no gain).
-constexpr int kFilterMinP = 6;
-constexpr int kFilterMinK = 15;
-constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane masks
+// Per-wave LDS pool of the rebuilding kernel: its queue (fewer than 64 entries
+// wait when a pair of block tiles adds its at most 2 x 1024) or, with the
+// record stage, the records, their queue and the per-slot threshold data.
+constexpr int kPoolWords = 128 + 2 * 1024;
 // P = 4 in the rebuilding kernel keeps walk survivors as records (16 bounds
 // and a meta word each) in its per-wave pool: 16 records waiting after a pair
 // of block tiles, rounds of 32 records (at most 512 queued seeds each). Only
@@ -74,13 +73,14 @@ constexpr int kMaskCheckMinP = 5;  // rungs that queue passing seeds by lane mas
 // records save (measured on 2.1 M blocks: (8..10,4) 4-7 % slower, (11,4)
 // even, (12,4) 8 % slower, (13..16,4) 2.5-5 % faster, (20,4) 5 % faster).
 constexpr int kRecordP = 4;
+constexpr bool kRemTable = false;   // the rebuilding kernel steps the LFSR
 constexpr int kRecordMinK = 13;
 constexpr int kRecFlushR = 16;
 constexpr int kRecCapR = kRecFlushR + 64;
 constexpr int kRecRound = 32;
 constexpr int kRecQueueWords = 64 + kRecRound * 16;
 static_assert(kRecQueueWords % 4 == 0, "records start 16-byte aligned");
-static_assert(kRecQueueWords + 17 * kRecCapR + 128 + 64 <= kQCapFiltered,
+static_assert(kRecQueueWords + 17 * kRecCapR + 128 + 64 <= kPoolWords,
               "the record stage fits the per-wave pool");
 constexpr int kBlocksPerWG = kWaves * kSlots;
 
@@ -150,6 +150,7 @@ struct MfmaArgs {
   int rung;
   int K;
   uint32_t mask;
+  const uint32_t* ub;
   const double* pinv64;
   const half8* pi16;
   int64_t ntiles;
@@ -194,6 +195,27 @@ SEEDQ_INLINE floatx16 bounds(const half8& a0, const half8& a1, const half8& a2, 
   acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b[1], acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b[2], acc, 0, 0, 0);
   return acc;
+}
+
+// Complement screen (P >= kComplementMinP): the projections d_c = 2^8 n_c^T w
+// of a block on the M complement vectors of 32 seeds are M products with K =
+// 16 (the hi and lo parts of 2^8 n_c against the block's fp16 weights, given
+// twice), and -sum_c d_c^2 is returned so that the max-fold, the records and
+// the pilot treat it like the quadratic form's bound: larger passes.
+template <int M>
+SEEDQ_INLINE floatx16 complement_screen(const half8 (&a)[M], const half8& b) {
+  floatx16 d[M];
+#pragma unroll
+  for (int c = 0; c < M; ++c) d[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[c], b, floatx16{}, 0, 0, 0);
+  floatx16 v;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    float r = -(d[0][j] * d[0][j]);
+#pragma unroll
+    for (int c = 1; c < M; ++c) r = fmaf(-d[c][j], d[c][j], r);
+    v[j] = r;
+  }
+  return v;
 }
 
 // Seed of accumulator j of a lane in half h of the wave, for tile seedbase.
@@ -276,6 +298,7 @@ template <int P>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3)))
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
+                   const uint32_t* __restrict__ ub,
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
@@ -312,9 +335,19 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   const int64_t wave_base = (int64_t(blockIdx.x) * kWaves + wave) * kSlots;
   if (wave_base >= count) return;  // wave-uniform; waves never synchronise
   const uint32_t nseeds = uint32_t((int64_t(1) << K) - 1);
+  // quadratic form: 3 A and 3 B fragments per tile; complement screen: M A
+  // fragments (one per complement vector) and one B fragment (the weights)
+  constexpr int M = complement_dims(P);
+  constexpr int NA = M > 0 ? M : 3;
+  constexpr int NB = M > 0 ? 1 : 3;
+  constexpr int64_t kTileFrags = NA * 64;   // half8 per seed tile of A fragments
+  auto screen = [&](const half8 (&a)[NA], const half8 (&b)[NB]) __attribute__((always_inline)) {
+    if constexpr (M > 0) return complement_screen<M>(a, b[0]);
+    else return bounds(a[0], a[1], a[2], b);
+  };
 
   // ---------------------------------------------------------------- prologue
-  half8 bop[kNB][3];
+  half8 bop[kNB][NB];
   float thr[kNB];
   bool active[kNB], valid[kNB];
 #pragma unroll
@@ -336,17 +369,34 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       ww = fmaf(ws[i], ws[i], ww);
     }
     thr[nt] = active[nt] ? -INFINITY : INFINITY;
-    bop[nt][0] = b_fragment<0>(ws, h);
-    bop[nt][1] = b_fragment<1>(ws, h);
-    bop[nt][2] = b_fragment<2>(ws, h);
+    if constexpr (M > 0) {
+#pragma unroll
+      for (int e = 0; e < kC; ++e) bop[nt][0][e] = _Float16(ws[e]);
+    } else {
+      bop[nt][0] = b_fragment<0>(ws, h);
+      bop[nt][1] = b_fragment<1>(ws, h);
+      bop[nt][2] = b_fragment<2>(ws, h);
+    }
     if (h == 0) {
       // a later chunk starts from the best so far (error in carry, seed in
       // seed_out); the first one from none
       best[nt * 32 + n] = chunk > 0 && valid[nt] ? carry[b] : ~0ull;
       if (chunk == 0 && valid[nt]) seed_out[b] = ~0u;
       blk[nt * 32 + n] = int32_t(b);
-      // thresholds live in accumulator units (both operands carry 2^12)
-      slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+      if constexpr (M > 0) {
+        // sqrt(M) times the bound on the error of each computed projection,
+        // in accumulator units (kComplementScale): fp16 rounding of the
+        // weights (2^-11 relative each, Cauchy-Schwarz with |n_c| = 1) plus
+        // that of the hi/lo complement vector (2^-22 relative, 2^-25 for
+        // subnormal parts) and the fp32 accumulation of 16 exact products,
+        // all under 2^-11 (1 + 2^-7) |w| + 2^-20; |w| <= sqrt(ww) (1 + 2^-20)
+        const float norm = sqrtf(ww) * (1.0f + 0x1p-20f);
+        slot_thr[nt * 32 + n] = sqrtf(float(M)) * (1.0f + 0x1p-20f) * kComplementScale *
+                                (0x1p-11f * (1.0f + 0x1p-7f) * norm + 0x1p-20f);
+      } else {
+        // thresholds live in accumulator units (both operands carry 2^12)
+        slot_thr[nt * 32 + n] = ww * one_minus_gamma * (kOperandScale * kOperandScale);
+      }
       slot_ex[nt * 32 + n] = int16_t(ex);
     }
   }
@@ -358,8 +408,22 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   auto slot_threshold = [&](int s) __attribute__((always_inline)) {
     const unsigned long long key = best[s];
     if (key == ~0ull) return -INFINITY;
-    return slot_thr[s] - __double2float_ru(ldexp(__longlong_as_double((long long)key),
-                                                 24 - 2 * int(slot_ex[s])));
+    if constexpr (M > 0) {
+      // a seed whose residual r_LS(w) is at most the best error b has computed
+      // projections of norm <= 2^8 sqrt(b 2^-2ex) + slot_thr (triangle
+      // inequality over the M of them), so their fp32 sum of squares (within
+      // 2^-20 of its value) is at most T = (2^8 sqrt(b 2^-2ex) + slot_thr)^2
+      // (1 + 2^-19). Evaluated in fp32 and rounded up by the factors below:
+      // the nearest-rounded conversion (2^-24 relative, 2^-150 absolute below
+      // the normal range), sqrtf (1 ulp) and each later rounding (2^-24).
+      const float bs = float(ldexp(__longlong_as_double((long long)key), -2 * int(slot_ex[s])));
+      const float rb = fmaf(sqrtf(bs), 1.0f + 0x1p-21f, 0x1p-62f);
+      const float t = fmaf(rb, kComplementScale, slot_thr[s]) * (1.0f + 0x1p-22f);
+      return -(t * t * (1.0f + 0x1p-18f));
+    } else {
+      return slot_thr[s] - __double2float_ru(ldexp(__longlong_as_double((long long)key),
+                                                   24 - 2 * int(slot_ex[s])));
+    }
   };
   auto refresh = [&]() __attribute__((always_inline)) {
     __threadfence_block();
@@ -390,7 +454,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
           float w[kC];
           load_block(W, b, true, w);
           int qe, q[P];
-          err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          err = exact_eval<P, (M > 0)>(w, pinv64 + int64_t(seed - 1) * (P * kC),
+                                       ub + int64_t(seed - 1) * basis_words(K, P), seed, K, mask,
+                                       qe, q);
           if (ent & kFinal) {
             seed_out[b] = seed;
             exp_out[b] = uint8_t(qe);
@@ -469,10 +535,12 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   if (chunk > 0) {
     refresh();
   } else {
-    const half8 a0 = A[lane], a1 = A[64 + lane], a2 = A[128 + lane];
+    half8 a[NA];
+#pragma unroll
+    for (int t = 0; t < NA; ++t) a[t] = A[64 * t + lane];
 #pragma unroll
     for (int nt = 0; nt < kNB; ++nt) {
-      const floatx16 acc = bounds(a0, a1, a2, bop[nt]);
+      const floatx16 acc = screen(a, bop[nt]);
       const float mx = fold_max(acc);
       int jb = 15;
 #pragma unroll
@@ -511,8 +579,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // One seed tile against the four block tiles: two block tiles at a time,
   // six products to the matrix core, then the folds, one branch per pair.
   // Before each block tile's records at most kRecCap - 64 are waiting.
-  auto tile = [&](const half8& a0, const half8& a1, const half8& a2, int64_t T)
-                  __attribute__((always_inline)) {
+  auto tile = [&](const half8 (&a)[NA], int64_t T) __attribute__((always_inline)) {
     const uint32_t t32 = uint32_t(T);
 #pragma unroll
     for (int pr = 0; pr < 2; ++pr) {
@@ -520,8 +587,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       // its products start ahead of the other waves' folds (measured +0.5 to
       // +1.1 % at (16,3); the rebuilding kernel measured slower with it)
       __builtin_amdgcn_s_setprio(1);
-      const floatx16 acc0 = bounds(a0, a1, a2, bop[2 * pr]);
-      const floatx16 acc1 = bounds(a0, a1, a2, bop[2 * pr + 1]);
+      const floatx16 acc0 = screen(a, bop[2 * pr]);
+      const floatx16 acc1 = screen(a, bop[2 * pr + 1]);
       __builtin_amdgcn_s_setprio(0);
       const bool p0 = fold_max(acc0) >= thr[2 * pr];
       const bool p1 = fold_max(acc1) >= thr[2 * pr + 1];
@@ -541,23 +608,22 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // Chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
   const int64_t T0 = int64_t(chunk) * ntiles / nchunks, T1 = int64_t(chunk + 1) * ntiles / nchunks;
   const int64_t last = T1 - 1;
-  half8 x0 = A[T0 * 192 + lane], x1 = A[T0 * 192 + 64 + lane], x2 = A[T0 * 192 + 128 + lane];
-  half8 y0, y1, y2;
+  half8 x[NA], y[NA];
+#pragma unroll
+  for (int t = 0; t < NA; ++t) x[t] = A[T0 * kTileFrags + 64 * t + lane];
   for (int64_t T = T0; T < T1; T += 2) {
     {
-      const half8* An = A + (T + 1 < last ? T + 1 : last) * 192;
-      y0 = An[lane];
-      y1 = An[64 + lane];
-      y2 = An[128 + lane];
+      const half8* An = A + (T + 1 < last ? T + 1 : last) * kTileFrags;
+#pragma unroll
+      for (int t = 0; t < NA; ++t) y[t] = An[64 * t + lane];
     }
-    tile(x0, x1, x2, T);
+    tile(x, T);
     {
-      const half8* An = A + (T + 2 < last ? T + 2 : last) * 192;
-      x0 = An[lane];
-      x1 = An[64 + lane];
-      x2 = An[128 + lane];
+      const half8* An = A + (T + 2 < last ? T + 2 : last) * kTileFrags;
+#pragma unroll
+      for (int t = 0; t < NA; ++t) x[t] = An[64 * t + lane];
     }
-    if (T + 1 < T1) tile(y0, y1, y2, T + 1);
+    if (T + 1 < T1) tile(y, T + 1);
   }
   process();
   evaluate(1);
@@ -595,7 +661,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   evaluate(1);
 }
 
-// The same search for P >= 4, where the fp64 evaluation needs more registers:
+// The same search at P = 4, where the fp64 evaluation needs more registers:
 // the block data (B fragments and thresholds) and the seed-tile fragments are
 // rebuilt from W, the keys and the projector stack after every evaluation
 // batch, so none of it is live across that code and the kernel fits four waves
@@ -604,8 +670,9 @@ template <int P, bool kRec>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
 search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
-                   const double* __restrict__ pinv64, const float* __restrict__ q32,
-                   const half8* __restrict__ pi16, int64_t ntiles, float one_minus_gamma,
+                   const uint32_t* __restrict__ ub,
+                   const double* __restrict__ pinv64, const half8* __restrict__ pi16,
+                   int64_t ntiles, float one_minus_gamma,
                    uint32_t* __restrict__ seed_out, uint8_t* __restrict__ exp_out,
                    int8_t* __restrict__ q_out, float* __restrict__ err_out, int nchunks,
                    int chunk, unsigned long long* __restrict__ carry) {
@@ -615,7 +682,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   static_assert(!kRec || P == kRecordP, "records only at P = 4");
   __shared__ unsigned long long best_all[kWaves][kSlots];
   __shared__ int32_t blk_all[kWaves][kSlots];
-  __shared__ __attribute__((aligned(16))) uint32_t pool_all[kWaves][kQCapFiltered];
+  __shared__ __attribute__((aligned(16))) uint32_t pool_all[kWaves][kPoolWords];
 
   const int lane = threadIdx.x & 63;
   // wave-uniform, so that the per-wave LDS addresses are scalar
@@ -712,79 +779,15 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
     }
   };
 
-  // The queue holds nf entries that passed the residual filter below (at the
-  // bottom) and qcount - nf new ones above them (wave-uniform counts).
-  int qcount = 0, nf = 0;
-  // Residual filter of the new entries: the least-squares residual is
-  // recomputed in fp32 from the orthonormal basis, ||w||^2 - ||Q_s^T w||^2,
-  // with a margin of 2^-16 ||w||^2 for its rounding instead of the matrix
-  // core's gamma. An entry that can still reach its block's best error moves
-  // down to the filtered region; the others are dropped, as are no-op entries
-  // (seed 0).
-  auto filter = [&]() __attribute__((always_inline)) {
-    if (P < kFilterMinP || K < kFilterMinK) {
-      nf = qcount;  // every entry goes to the exact evaluation (no-op entries skip it)
-      return;
-    }
-    __threadfence_block();
-    for (int i = nf; i < qcount; i += 64) {
-      const int e = qcount - i < 64 ? qcount - i : 64;
-      uint32_t ent = 0u;
-      bool keep = false;
-      if (lane < e) {
-        ent = queue[i + lane];
-        const uint32_t seed = ent >> 8;
-        const int slot = int(ent & 0x7Fu);
-        const unsigned long long key = best[slot];
-        keep = seed != 0u;
-        if (keep && !(ent & kFinal) && key != ~0ull) {
-          float w[kC];
-          load_block(W, blk[slot], true, w);
-          float amax = 0.f;
-#pragma unroll
-          for (int k = 0; k < kC; ++k) amax = fmaxf(amax, fabsf(w[k]));
-          const int ex = ilogbf(amax);  // queued blocks are not all zero
-          float ws[kC], ww = 0.f;
-#pragma unroll
-          for (int k = 0; k < kC; ++k) {
-            ws[k] = ldexpf(w[k], -ex);
-            ww = fmaf(ws[k], ws[k], ww);
-          }
-          const float4* Qs = reinterpret_cast<const float4*>(q32 + int64_t(seed - 1) * (P * kC));
-          float ss = 0.f;
-#pragma unroll
-          for (int p = 0; p < P; ++p) {
-            const float4 a = Qs[2 * p], b = Qs[2 * p + 1];
-            float c = a.x * ws[0];
-            c = fmaf(a.y, ws[1], c);
-            c = fmaf(a.z, ws[2], c);
-            c = fmaf(a.w, ws[3], c);
-            c = fmaf(b.x, ws[4], c);
-            c = fmaf(b.y, ws[5], c);
-            c = fmaf(b.z, ws[6], c);
-            c = fmaf(b.w, ws[7], c);
-            ss = fmaf(c, c, ss);
-          }
-          const float bu = __double2float_ru(ldexp(__longlong_as_double((long long)key), -2 * ex)) *
-                           (1.0f + 0x1p-20f);
-          keep = ss >= ww * (1.0f - 0x1p-16f) - bu;
-        }
-      }
-      const uint64_t mk = ballot(keep);
-      if (keep) queue[nf + lanes_below(mk)] = ent;
-      nf += __popcll(mk);
-    }
-    qcount = nf;
-    __threadfence_block();
-  };
-  // Evaluate the top min(64, nf) filtered entries, one per lane, until fewer
+  int qcount = 0;  // wave-uniform
+  // Evaluate the top min(64, qcount) queued entries, one per lane, until fewer
   // than min_batch remain; after any evaluation rebuild the block data and
   // thresholds. Returns whether it evaluated (wave-uniform).
   auto exact_with = [&](int min_batch, auto&& rebuild) __attribute__((always_inline)) {
     bool ran = false;
-    while (nf >= min_batch && nf > 0) {
-      const int e = nf < 64 ? nf : 64;
-      const int base = nf - e;
+    while (qcount >= min_batch && qcount > 0) {
+      const int e = qcount < 64 ? qcount : 64;
+      const int base = qcount - e;
       bool mine = false;
       uint32_t seed = 0u;
       int slot = 0;
@@ -799,7 +802,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
           float w[kC];
           load_block(W, b, true, w);
           int qe, q[P];
-          err = exact_eval<P>(w, pinv64 + int64_t(seed - 1) * (P * kC), seed, K, mask, qe, q);
+          err = exact_eval<P, kRemTable>(w, pinv64 + int64_t(seed - 1) * (P * kC),
+                                         ub + int64_t(seed - 1) * basis_words(K, P), seed, K,
+                                         mask, qe, q);
           if (ent & kFinal) {
             seed_out[b] = seed;
             exp_out[b] = uint8_t(qe);
@@ -818,10 +823,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
         }
       }
       record_best(best, seed_out, slot, b, err, seed, mine);
-      nf = base;
+      qcount = base;
       ran = true;
     }
-    qcount = nf;
     if (ran) {
       __threadfence_block();
       rebuild();
@@ -876,10 +880,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
         }
       }
       nrec = base;
-      if (qcount >= 64) {
-        nf = qcount;
-        exact_with(64, rebuild);
-      }
+      if (qcount >= 64) exact_with(64, rebuild);
     }
   };
   // Lanes of block tile nt whose fold passed store their 16 bounds as records.
@@ -897,10 +898,6 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       meta[r] = (T << 8) | ((l >> 5) << 7) | (uint32_t(nt * 32) + (l & 31u));
     }
     nrec += __popcll(mk);
-  };
-  auto flush = [&](int min_batch) __attribute__((always_inline)) {
-    filter();
-    exact(min_batch);
   };
 
   const half8* A = pi16;
@@ -928,48 +925,30 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       if (put) queue[qcount + lanes_below(mk)] = (sd << 8) | uint32_t(nt * 32 + n);
       qcount += __popcll(mk);
     }
-    flush(1);
+    exact(1);
   }
 
   // ---------------------------------------------------------------- seed walk
-  // Queue the candidates of block tile nt whose bound passes. At most 1024 per
-  // block tile; fewer than 64 are queued before a pair of block tiles, so the
-  // 2 x 1024 of one pair always fit.
-  // At P >= 5 a few percent of the candidates pass, so most of the 16 seeds of
-  // a tile have a passing lane: there each lane builds its mask of passing
-  // seeds and queues one set bit per round (at P = 6 only for K >= 15, where
-  // it measured faster). Otherwise one ballot per seed.
-  const bool mask_check = P >= kMaskCheckMinP && (P < kFilterMinP || K >= kFilterMinK);
+  // Queue the candidates of block tile nt whose bound passes, one ballot per
+  // seed. At most 1024 per block tile; fewer than 64 are queued before a pair
+  // of block tiles, so the 2 x 1024 of one pair always fit.
   auto check = [&](auto ntc, const floatx16& acc, bool any, uint32_t seedbase)
                    __attribute__((always_inline)) {
     constexpr int nt = decltype(ntc)::value;
     if (ballot(any) == 0ull) return;
-    if (P >= kMaskCheckMinP && mask_check) {
-      uint32_t m = 0u;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) m |= (acc[j] >= thr[nt] ? 1u : 0u) << j;
-      for (;;) {
-        const uint64_t mk = ballot(m != 0u);
-        if (mk == 0ull) break;
-        if (m != 0u) {
-          const uint32_t seed = seed_of(seedbase, __builtin_ctz(m), h);
-          queue[qcount + lanes_below(mk)] =
-              ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
-          m &= m - 1u;
-        }
-        qcount += __popcll(mk);
-      }
-      return;
-    }
+    // half and slot recomputed here, so that the 16 seed offsets and the slot
+    // are not hoisted out of the walk and kept live (or spilled) across it
+    const uint32_t l = lane_now();
+    const int hh = int(l >> 5);
+    const uint32_t slot = uint32_t(nt * 32) + (l & 31u);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const bool pass = acc[j] >= thr[nt];
       const uint64_t mk = ballot(pass);
       if (mk != 0ull) {
         if (pass) {
-          const uint32_t seed = seed_of(seedbase, j, h);
-          queue[qcount + lanes_below(mk)] =
-              ((seed <= nseeds ? seed : 0u) << 8) | uint32_t(nt * 32 + n);
+          const uint32_t seed = seed_of(seedbase, j, hh);
+          queue[qcount + lanes_below(mk)] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
         }
         qcount += __popcll(mk);
       }
@@ -984,9 +963,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // Seed-tile fragments; the index is clamped to the last tile so that every
   // load is unconditional and each wait covers only the tile it is for.
   // Chunk `chunk` walks tiles [T0, T1) (at least 8 of them).
-  const int64_t T0 = int64_t(chunk) * ntiles / nchunks, T1 = int64_t(chunk + 1) * ntiles / nchunks;
-  const int64_t last = T1 - 1;
-  auto load_tile = [&](int64_t T, half8 (&f)[3]) __attribute__((always_inline)) {
+  const int T0 = int(int64_t(chunk) * ntiles / nchunks), T1 = int(int64_t(chunk + 1) * ntiles / nchunks);
+  const int last = T1 - 1;   // 32-bit tile indices (ntiles < 2^19), kept scalar
+  auto load_tile = [&](int T, half8 (&f)[3]) __attribute__((always_inline)) {
     const half8* At = A + (T < last ? T : last) * 192;
     f[0] = At[lane];
     f[1] = At[64 + lane];
@@ -997,7 +976,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // at a time: six products to the matrix core, then the folds, one branch per
   // pair. An exact evaluation rebuilds the block data and reloads both this
   // tile's fragments and those of the other set (tile To, in o).
-  auto tile = [&](half8 (&c)[3], int64_t T, half8 (&o)[3], int64_t To)
+  auto tile = [&](half8 (&c)[3], int T, half8 (&o)[3], int To)
                   __attribute__((always_inline)) {
     const uint32_t seedbase = uint32_t(T) * 32u + 1u;
     {
@@ -1020,12 +999,9 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
         } else {
           check(I0{}, acc0, p0, seedbase);
           check(I1{}, acc1, p1, seedbase);
-          if (qcount - nf >= 64) {
-            filter();
-            if (exact(64)) {
-              load_tile(T, c);
-              load_tile(To, o);
-            }
+          if (qcount >= 64 && exact(64)) {
+            load_tile(T, c);
+            load_tile(To, o);
           }
         }
       }
@@ -1049,10 +1025,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
         } else {
           check(I2{}, acc2, p2, seedbase);
           check(I3{}, acc3, p3, seedbase);
-          if (qcount - nf >= 64) {
-            filter();
-            if (exact(64)) load_tile(To, o);
-          }
+          if (qcount >= 64 && exact(64)) load_tile(To, o);
         }
       }
     }
@@ -1061,14 +1034,14 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   // Two fragment sets in turn: one tile is loaded while the other is screened.
   half8 x[3], y[3];
   load_tile(T0, x);
-  for (int64_t T = T0; T < T1; T += 2) {
+  for (int T = T0; T < T1; T += 2) {
     load_tile(T + 1, y);
     tile(x, T, y, T + 1);
     load_tile(T + 2, x);
     if (T + 1 < T1) tile(y, T + 1, x, T + 2);
   }
   if constexpr (kRec) process(setup);
-  flush(1);
+  exact(1);
 
   // ---------------------------------------------------------------- results
   // A chunk before the last hands its best errors on to the next launch (the
@@ -1101,7 +1074,7 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
       if (err_out) err_out[b] = 0.f;
     }
   }
-  flush(1);
+  exact(1);
 }
 
 // ---------------------------------------------------------------- seed chunks
@@ -1142,8 +1115,9 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.rung = rung;
   a.K = K;
   a.mask = lfsr_mask(K);
+  a.ub = reinterpret_cast<const uint32_t*>(base + L.off_ub);
   a.pinv64 = reinterpret_cast<const double*>(base + L.off_pinv64);
-  a.pi16 = reinterpret_cast<const half8*>(base + L.off_pi16);
+  a.pi16 = reinterpret_cast<const half8*>(base + (complement_dims(P) > 0 ? L.off_nc16 : L.off_pi16));
   a.ntiles = L.ntiles;
   const double gamma = std::sqrt(double(P)) * 0x1p-10 * (1.0 + 0x1p-6) + 0x1p-14;
   a.one_minus_gamma = float(1.0 - gamma);
@@ -1159,18 +1133,17 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   unsigned long long* carry = reinterpret_cast<unsigned long long*>(d_q);
   const dim3 grid = dim3(unsigned(blocks), 1u, 1u);
   for (int64_t c = 0; c < nseq; ++c) {
-    if constexpr (P >= 4) {
+    if constexpr (P == 4) {
       auto kern = search_mfma_remat_kernel<P, false>;
       if constexpr (P == kRecordP)
         if (K >= kRecordMinK) kern = search_mfma_remat_kernel<P, true>;
       hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0,
-                         stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64,
-                         reinterpret_cast<const float*>(base + L.off_q32), a.pi16, a.ntiles,
-                         a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out, int(nseq),
-                         int(c), carry);
+                         stream, a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.ub, a.pinv64,
+                         a.pi16, a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out,
+                         a.err_out, int(nseq), int(c), carry);
     } else {
       hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
-                         a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.pinv64, a.pi16,
+                         a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.ub, a.pinv64, a.pi16,
                          a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
                          int(nseq), int(c), carry);
     }

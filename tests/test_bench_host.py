@@ -23,7 +23,7 @@ def test_help_lists_every_mode():
     r = _run("--help")
     assert r.returncode == 0
     for flag in ("--steps", "--warmup", "--workload", "--decoder", "--grid", "--frontend",
-                 "--no-cpu-baseline", "--cpu-seconds"):
+                 "--no-cpu-baseline", "--cpu-seconds", "--row-tiles"):
         assert flag in r.stdout, flag
 
 
