@@ -293,9 +293,22 @@ static_assert(kSlots <= 128, "slot must fit 7 bits");
 constexpr int kRecFlush = 32;                 // records waiting after a pair of block tiles
 constexpr int kRecCap = kRecFlush + 64;       // one block tile adds at most 64
 constexpr int kQCapRec = 64 + 64 * 16;        // < 64 waiting + one round of 64 records
+// At P = 6 (two complement vectors) records hold their bounds as fp16 (16 x
+// 2 bytes: two float4 of storage instead of four), which brings the kernel's
+// LDS to 40 KB and, with at most 128 VGPRs, four waves per SIMD (measured on
+// 2.1 M blocks: (14..16,6) 5-6 % faster; at P = 5 the register limit spills
+// and measured 18 % slower). The values -sum d^2 are scaled by 2^-8 into fp16
+// range (|d| < 2^11) and rounded toward zero, i.e. up, so that a stored bound
+// is never below the computed one.
+__host__ __device__ constexpr bool half_records(int P) { return complement_dims(P) == 2; }
+template <int P>
+constexpr int kRecVecs = half_records(P) ? 2 : 4;
+constexpr float kRecScale = 0x1p-8f;
+typedef __fp16 fp16x2 __attribute__((ext_vector_type(2)));
 
 template <int P>
-__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ void __launch_bounds__(kWaves * 64)
+__attribute__((amdgpu_waves_per_eu(half_records(P) ? 4 : 3)))
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
                    const uint32_t* __restrict__ ub,
@@ -310,7 +323,8 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // power-of-two scaling of the block: ilogb of its largest |w_i|, down to -149
   // for fp32 subnormals, so 16 bits
   __shared__ int16_t ex_all[kWaves][kSlots];
-  __shared__ float4 rec_all[kWaves][kRecCap][4];   // 16 bounds per record
+  // 16 bounds per record: fp32, or fp16 at P = 6 (see half_records)
+  __shared__ float4 rec_all[kWaves][kRecCap][kRecVecs<P>];
   __shared__ uint32_t meta_all[kWaves][kRecCap];
   __shared__ uint32_t queue_all[kWaves][kQCapRec];
 
@@ -323,7 +337,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   int32_t* blk = blk_all[wave];
   float* slot_thr = thr_base_all[wave];
   int16_t* slot_ex = ex_all[wave];
-  float4 (*rec)[4] = rec_all[wave];
+  float4 (*rec)[kRecVecs<P>] = rec_all[wave];
   uint32_t* meta = meta_all[wave];
   uint32_t* queue = queue_all[wave];
 
@@ -493,17 +507,39 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       const bool live = lane < e;
       uint32_t m = 0u;
       float t = INFINITY;
-      float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0, r2 = r0, r3 = r0;
-      if (live) {
-        m = meta[base + lane];
-        t = slot_threshold(int(m & 0x7Fu));
-        r0 = rec[base + lane][0];
-        r1 = rec[base + lane][1];
-        r2 = rec[base + lane][2];
-        r3 = rec[base + lane][3];
-      }
-      const float bnd[16] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w,
+      float bnd[16];
+      if constexpr (half_records(P)) {
+        float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0;
+        if (live) {
+          m = meta[base + lane];
+          // the stored bounds are scaled by 2^-8; so is the threshold, less
+          // 2^-140 for the rounding of the scaling below the normal range
+          t = fmaf(slot_threshold(int(m & 0x7Fu)), kRecScale, -0x1p-140f);
+          r0 = rec[base + lane][0];
+          r1 = rec[base + lane][1];
+        }
+        const float r[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const fp16x2 v = __builtin_bit_cast(fp16x2, r[k]);
+          bnd[2 * k] = float(v[0]);
+          bnd[2 * k + 1] = float(v[1]);
+        }
+      } else {
+        float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0, r2 = r0, r3 = r0;
+        if (live) {
+          m = meta[base + lane];
+          t = slot_threshold(int(m & 0x7Fu));
+          r0 = rec[base + lane][0];
+          r1 = rec[base + lane][1];
+          r2 = rec[base + lane][2];
+          r3 = rec[base + lane][3];
+        }
+        const float r[16] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w,
                              r2.x, r2.y, r2.z, r2.w, r3.x, r3.y, r3.z, r3.w};
+#pragma unroll
+        for (int k = 0; k < 16; ++k) bnd[k] = r[k];
+      }
       const uint32_t seedbase = (m >> 8) * 32u + 1u;
       const int hh = int((m >> 7) & 1u);
       const uint32_t slot = m & 0x7Fu;
@@ -566,10 +602,20 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     if (mk == 0ull) return;
     if (pass) {
       const int r = nrec + lanes_below(mk);
-      rec[r][0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      rec[r][1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-      rec[r][2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
-      rec[r][3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      if constexpr (half_records(P)) {
+        float pk[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          pk[k] = __builtin_bit_cast(float, __builtin_amdgcn_cvt_pkrtz(acc[2 * k] * kRecScale,
+                                                                       acc[2 * k + 1] * kRecScale));
+        rec[r][0] = make_float4(pk[0], pk[1], pk[2], pk[3]);
+        rec[r][1] = make_float4(pk[4], pk[5], pk[6], pk[7]);
+      } else {
+        rec[r][0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        rec[r][1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+        rec[r][2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+        rec[r][3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      }
       meta[r] = (T << 8) | (uint32_t(h) << 7) | uint32_t(nt * 32 + n);
     }
     nrec += __popcll(mk);
@@ -966,10 +1012,14 @@ search_mfma_remat_kernel(const float* __restrict__ W, int64_t nblocks, const int
   const int T0 = int(int64_t(chunk) * ntiles / nchunks), T1 = int(int64_t(chunk + 1) * ntiles / nchunks);
   const int last = T1 - 1;   // 32-bit tile indices (ntiles < 2^19), kept scalar
   auto load_tile = [&](int T, half8 (&f)[3]) __attribute__((always_inline)) {
+    // without records the lane's offset is recomputed here, so that no 64-bit
+    // per-lane address stays live (or spilled) across the walk (with records
+    // the same change makes the allocator spill elsewhere)
     const half8* At = A + (T < last ? T : last) * 192;
-    f[0] = At[lane];
-    f[1] = At[64 + lane];
-    f[2] = At[128 + lane];
+    const uint32_t l = kRec ? uint32_t(lane) : lane_now();
+    f[0] = At[l];
+    f[1] = At[64 + l];
+    f[2] = At[128 + l];
   };
 
   // Seed tile T (fragments c) against the four block tiles, two block tiles
