@@ -485,10 +485,12 @@ def compress_row_tiles(W_host, bases: list, rung_of_block=None, row_tiles: int =
     GPU in ``row_tiles`` contiguous row ranges (blocks are independent once the
     rungs are planned, so every tile is one seedq_compress call on its rows and
     their slice of the rung array). W_host: torch fp32 [nrows, ncols] on the
-    host, pinned for asynchronous copies. Two tile buffers alternate: the copy
-    of the next tile (on a copy stream) overlaps the search of this one (on the
-    current stream). Outputs as ``compress`` (device tensors); only two tiles of
-    W are ever resident in device memory."""
+    host, pinned for asynchronous copies. Two tile buffers alternate, each with
+    its own compute stream (the current one and a second) and workspace: the
+    copy of the next tile (on a copy stream) overlaps the search of this one,
+    and consecutive searches overlap each other's tails. Outputs as
+    ``compress`` (device tensors), complete on the current stream; only two
+    tiles of W are ever resident in device memory."""
     import torch
     nrows, ncols = W_host.shape
     G = ncols // SEEDQ_BLOCK
@@ -502,14 +504,18 @@ def compress_row_tiles(W_host, bases: list, rung_of_block=None, row_tiles: int =
     rows_max = max(bounds[t + 1] - bounds[t] for t in range(row_tiles))
     bufs = [torch.empty((rows_max, ncols), dtype=torch.float32, device=dev) for _ in range(2)]
     nws = seedq_compress_workspace_bytes(rows_max, ncols, SEEDQ_BLOCK, len(bases))
-    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev) if nws else None
-    compute = torch.cuda.current_stream()
+    wss = [torch.empty(max(nws, 256), dtype=torch.uint8, device=dev) if nws else None
+           for _ in range(2)]
+    current = torch.cuda.current_stream()
+    computes = [current, torch.cuda.Stream(device=dev)]
     copy = torch.cuda.Stream(device=dev)
     copied = [torch.cuda.Event() for _ in range(2)]
     searched = [torch.cuda.Event() for _ in range(2)]
-    # the tile buffers come from the current stream's pool, whose pending work
-    # may still read the memory they reuse: copies start after that work
-    copy.wait_stream(compute)
+    # the buffers come from the current stream's pool, whose pending work may
+    # still read the memory they reuse, and the rung array may still be being
+    # written there: the other streams start after that work
+    copy.wait_stream(current)
+    computes[1].wait_stream(current)
 
     def upload(t):
         r0, r1 = bounds[t], bounds[t + 1]
@@ -526,14 +532,18 @@ def compress_row_tiles(W_host, bases: list, rung_of_block=None, row_tiles: int =
         if t + 1 < row_tiles:
             upload(t + 1)
         k = t % 2
-        compute.wait_event(copied[k])
+        cs = computes[k]   # buffer k, workspace k and stream k go together
+        cs.wait_event(copied[k])
         if r1 > r0:
             b0, b1 = r0 * G, r1 * G
             seedq_compress(bufs[k][: r1 - r0], r1 - r0, ncols, SEEDQ_BLOCK,
                            None if rung_of_block is None else rung_of_block[b0:b1], bases,
                            seed[b0:b1], exp[b0:b1], q[b0:b1], None if err is None else err[b0:b1],
-                           ws, nws, compute)
-        searched[k].record(compute)
+                           wss[k], nws, cs)
+        searched[k].record(cs)
+    # everything after this call on the current stream (and the allocator's
+    # reuse of the buffers) comes after the second stream's searches
+    current.wait_stream(computes[1])
     return seed, exp, q, err
 
 

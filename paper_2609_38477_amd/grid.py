@@ -115,11 +115,32 @@ def mean_errors(err: dict) -> dict:
             for r, e in err.items()}
 
 
+def parse_rungs(text: str) -> tuple:
+    """Rungs named on the command line: "paper" (the 45-rung grid),
+    "rungshape" (the rungs of the rung-shape table and the reference rung) or
+    an explicit list "K,P;K,P;..." in the order to build them."""
+    if text == "paper":
+        return PAPER_GRID
+    if text == "rungshape":
+        return tuple(sorted(set(RUNGSHAPE_RUNGS) | {REFERENCE_RUNG}))
+    out = []
+    for item in text.split(";"):
+        parts = item.split(",")
+        if len(parts) != 2:
+            raise ValueError(f"rung {item!r} is not K,P")
+        out.append((int(parts[0]), int(parts[1])))
+    if not out or len(set(out)) != len(out):
+        raise ValueError(f"rung list {text!r} is empty or repeats a rung")
+    return tuple(out)
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="attn4096")
-    ap.add_argument("--rungs", choices=("paper", "rungshape"), default="paper")
+    ap.add_argument("--rungs", default="paper",
+                    help='"paper", "rungshape" or a list "K,P;K,P;..." (built in that order)')
     args = ap.parse_args(argv)
+    rungs = parse_rungs(args.rungs)
     import torch
     import os
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -131,12 +152,12 @@ def main(argv=None) -> int:
         return 2
     wl = synthetic.WORKLOADS[args.workload]
     W = torch.from_numpy(synthetic.workload_weights(wl)).cuda()
-    rungs = PAPER_GRID if args.rungs == "paper" else tuple(sorted(set(RUNGSHAPE_RUNGS) | {REFERENCE_RUNG}))
     build_grid(W, rungs=((8, 2),))  # warm-up: module load and first launch
     t0 = time.perf_counter()
     res = build_grid(W, rungs=rungs)
     wall = time.perf_counter() - t0
-    table = rungshape(res.err)
+    table = (rungshape(res.err, rungs=[r for r in RUNGSHAPE_RUNGS if r in res.err])
+             if REFERENCE_RUNG in res.err else [])
     me = mean_errors(res.err)
     per_rung = [{"rung": list(r), "rate_bpw": rate_bpw(*r), "search_ms": res.search_ms[r],
                  "bases_ms": res.bases_ms[r],

@@ -3,6 +3,7 @@ and the ratio summary against closed forms."""
 import os
 
 import numpy as np
+import pytest
 
 from paper_2609_38477_amd import grid
 
@@ -59,3 +60,12 @@ def test_rungshape_lognormal_ratio_and_zero_blocks():
     assert abs(r["q10"] / (1.5 * np.exp(-1.2815516 * s)) - 1) < 0.01
     assert abs(r["q90"] / (1.5 * np.exp(1.2815516 * s)) - 1) < 0.01
     assert abs(r["sd_log"] - s) < 0.005
+
+
+def test_parse_rungs_names_and_lists():
+    assert grid.parse_rungs("paper") == grid.PAPER_GRID
+    assert set(grid.parse_rungs("rungshape")) == set(grid.RUNGSHAPE_RUNGS) | {grid.REFERENCE_RUNG}
+    assert grid.parse_rungs("16,6;16,5;12,2") == ((16, 6), (16, 5), (12, 2))
+    for bad in ("", "16", "16,6;16,6", "16,6,1", "a,b"):
+        with pytest.raises(ValueError):
+            grid.parse_rungs(bad)
