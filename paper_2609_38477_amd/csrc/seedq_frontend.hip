@@ -7,8 +7,8 @@
 //                 partial sums added in a fixed order)
 //   column stats: max_i |W_ij| and the median of |W_ij| over the rows, by a
 //                 radix select on the bit patterns of |W| (non-negative floats
-//                 order like their bits), 8 bits per pass, per-column
-//                 histograms in LDS
+//                 order like their bits), three passes of 11, 10 and 10 bits,
+//                 per-column histograms in LDS
 //   E[silu(g)^2]: Gauss-Hermite quadrature per channel
 //   column permutation (gather or scatter) and fp16 column escape.
 // All sums are fp64; every result is independent of scheduling.
@@ -98,75 +98,141 @@ sq_gemv_t_total_kernel(const double* __restrict__ part, int64_t nchunks, int64_t
   out[c] = acc;
 }
 
-constexpr int kStatCols = 32;  // columns per workgroup
+// Column statistics: three passes of a radix select on the 31-bit patterns of
+// |W| (non-negative floats order like their bits), digits of 11, 10 and 10
+// bits, with per-column histograms in LDS. 8 columns per workgroup (64 KB of
+// histograms, two workgroups per CU), 32 row groups of threads per column.
+constexpr int kStatCols = 8;
+constexpr int kStatGroups = kThreads / kStatCols;   // 32 threads per column
+constexpr int kStatBins = 2048;                     // the first digit's bins
+constexpr int kStatSuper = 32;                      // workgroups per XCD-aware super-block
 
-// The k-th smallest |W[:, c]| (0-based) for the 32 columns of this workgroup:
-// four passes of an 8-bit radix select over the bit patterns, most significant
-// byte first. Returns the key for column threadIdx.x (threads < 32).
-__device__ uint32_t select_kth(const float* __restrict__ W, int64_t nrows, int64_t ncols,
-                               int64_t c0, int64_t k, uint32_t (*hist)[256], uint32_t* prefix_s,
-                               uint32_t* mask_s, int64_t* k_s) {
-  const int col = threadIdx.x & (kStatCols - 1);
-  const int grp = threadIdx.x / kStatCols;          // 8 row groups
-  const int64_t c = c0 + col;
-  if (threadIdx.x < kStatCols) {
-    prefix_s[col] = 0u;
-    mask_s[col] = 0u;
-    k_s[col] = k;
-  }
+// Finds, for every column of the workgroup, the bin of hist[col][0, nbins)
+// that holds the element of rank rank[col] (0-based), and the rank inside it:
+// each of the 32 threads of a column sums its run of nbins/32 bins, takes the
+// prefix of the runs before it, and the thread whose run holds the rank scans
+// it. Results in bin_s / rank_s; the caller synchronises.
+__device__ void find_rank(const uint32_t (*hist)[kStatBins], int nbins, const int64_t* rank,
+                          uint32_t (*part)[kStatGroups], uint32_t* bin_s, int64_t* rank_s) {
+  const int col = threadIdx.x % kStatCols, grp = threadIdx.x / kStatCols;
+  const int run = nbins / kStatGroups;
+  uint32_t sum = 0u;
+  for (int b = grp * run; b < (grp + 1) * run; ++b) sum += hist[col][b];
+  part[col][grp] = sum;
   __syncthreads();
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = threadIdx.x; i < kStatCols * 256; i += kThreads) hist[i / 256][i % 256] = 0u;
-    __syncthreads();
-    const uint32_t prefix = prefix_s[col], mask = mask_s[col];
-    if (c < ncols) {
-      for (int64_t r = grp; r < nrows; r += kThreads / kStatCols) {
-        const uint32_t key = __float_as_uint(W[r * ncols + c]) & 0x7FFFFFFFu;
-        if ((key & mask) == prefix) atomicAdd(&hist[col][(key >> shift) & 255u], 1u);
-      }
+  int64_t before = 0;
+  for (int g = 0; g < grp; ++g) before += part[col][g];
+  const int64_t k = rank[col];
+  if (k >= before && k < before + int64_t(sum)) {
+    int64_t kk = k - before;
+    int b = grp * run;
+    for (;; ++b) {
+      const int64_t n = hist[col][b];
+      if (kk < n) break;
+      kk -= n;
     }
-    __syncthreads();
-    if (threadIdx.x < kStatCols) {
-      int64_t kk = k_s[col];
-      uint32_t b = 0;
-      for (; b < 255u; ++b) {
-        const int64_t n = hist[col][b];
-        if (kk < n) break;
-        kk -= n;
-      }
-      k_s[col] = kk;
-      prefix_s[col] |= b << shift;
-      mask_s[col] |= 255u << shift;
-    }
-    __syncthreads();
+    bin_s[col] = uint32_t(b);
+    rank_s[col] = kk;
   }
-  return prefix_s[col];
 }
 
 __global__ void __launch_bounds__(kThreads)
 column_stats_kernel(const float* __restrict__ W, int64_t nrows, int64_t ncols,
                     double* __restrict__ maxabs, double* __restrict__ median) {
-  __shared__ uint32_t hist[kStatCols][256];
-  __shared__ uint32_t prefix_s[kStatCols], mask_s[kStatCols], mx_s[kStatCols];
-  __shared__ int64_t k_s[kStatCols];
-  const int64_t c0 = int64_t(blockIdx.x) * kStatCols;
-  const int col = threadIdx.x & (kStatCols - 1);
-  const int grp = threadIdx.x / kStatCols;
+  __shared__ uint32_t hist[kStatCols][kStatBins];
+  __shared__ uint32_t part[kStatCols][kStatGroups];
+  __shared__ uint32_t mx_s[kStatCols], above_s[kStatCols], bin_s[kStatCols], next_s[kStatCols];
+  __shared__ int64_t rank_s[kStatCols], k_s[kStatCols];
+  // XCD-aware column groups: workgroups are dispatched to the 8 XCDs in turn,
+  // so of 32 consecutive workgroups those on one XCD take the 4 neighbouring
+  // groups of 8 columns that share 128-byte lines of every row.
+  const int64_t b = blockIdx.x, b0 = b - b % kStatSuper;
+  const int64_t group = b0 + (b % 8) * 4 + (b % kStatSuper) / 8;
+  const int64_t c0 = group * kStatCols;
+  if (c0 >= ncols) return;   // the grid is rounded up to whole super-blocks
+  const int col = threadIdx.x % kStatCols, grp = threadIdx.x / kStatCols;
   const int64_t c = c0 + col;
-  if (threadIdx.x < kStatCols) mx_s[col] = 0u;
+  const bool live = c < ncols;
+  const float* Wc = W + (live ? c : c0);
+  const int64_t klo = (nrows - 1) / 2;
+
+  for (int i = threadIdx.x; i < kStatCols * kStatBins; i += kThreads) hist[i / kStatBins][i % kStatBins] = 0u;
+  if (threadIdx.x < kStatCols) {
+    mx_s[threadIdx.x] = 0u;
+    above_s[threadIdx.x] = 0xFFFFFFFFu;
+    next_s[threadIdx.x] = 0xFFFFFFFFu;
+    k_s[threadIdx.x] = klo;
+    bin_s[threadIdx.x] = 0u;     // columns past ncols find no rank: keep bins in range
+    rank_s[threadIdx.x] = 0;
+  }
   __syncthreads();
-  if (c < ncols) {
+
+  // pass 1: maximum and the histogram of bits 30..20
+  if (live) {
     uint32_t m = 0u;
-    for (int64_t r = grp; r < nrows; r += kThreads / kStatCols)
-      m = max(m, __float_as_uint(W[r * ncols + c]) & 0x7FFFFFFFu);
+    for (int64_t r = grp; r < nrows; r += kStatGroups) {
+      const uint32_t key = __float_as_uint(Wc[r * ncols]) & 0x7FFFFFFFu;
+      m = max(m, key);
+      atomicAdd(&hist[col][key >> 20], 1u);
+    }
     atomicMax(&mx_s[col], m);
   }
   __syncthreads();
-  const uint32_t lo = select_kth(W, nrows, ncols, c0, (nrows - 1) / 2, hist, prefix_s, mask_s, k_s);
-  uint32_t hi = lo;
-  if (nrows % 2 == 0)
-    hi = select_kth(W, nrows, ncols, c0, nrows / 2, hist, prefix_s, mask_s, k_s);
-  if (threadIdx.x < kStatCols && c < ncols) {
+  find_rank(hist, kStatBins, k_s, part, bin_s, rank_s);
+  __syncthreads();
+  const uint32_t d1 = bin_s[col] & (kStatBins - 1u);
+  if (threadIdx.x < kStatCols) k_s[threadIdx.x] = rank_s[threadIdx.x];
+  for (int i = threadIdx.x; i < kStatCols * kStatBins; i += kThreads) hist[i / kStatBins][i % kStatBins] = 0u;
+  __syncthreads();
+
+  // pass 2: bits 19..10 of the keys in the median's first-digit bin
+  if (live) {
+    for (int64_t r = grp; r < nrows; r += kStatGroups) {
+      const uint32_t key = __float_as_uint(Wc[r * ncols]) & 0x7FFFFFFFu;
+      if ((key >> 20) == d1) atomicAdd(&hist[col][(key >> 10) & 1023u], 1u);
+    }
+  }
+  __syncthreads();
+  find_rank(hist, 1024, k_s, part, bin_s, rank_s);
+  __syncthreads();
+  const uint32_t pre = (d1 << 10) | (bin_s[col] & 1023u);   // bits 30..10 of the median
+  if (threadIdx.x < kStatCols) k_s[threadIdx.x] = rank_s[threadIdx.x];
+  for (int i = threadIdx.x; i < kStatCols * 1024; i += kThreads) hist[i / 1024][i % 1024] = 0u;
+  __syncthreads();
+
+  // pass 3: bits 9..0 of the keys with that prefix, and the smallest key
+  // above the prefix (the upper middle value when the lower one is the
+  // largest key with it)
+  if (live) {
+    uint32_t above = 0xFFFFFFFFu;
+    for (int64_t r = grp; r < nrows; r += kStatGroups) {
+      const uint32_t key = __float_as_uint(Wc[r * ncols]) & 0x7FFFFFFFu;
+      if ((key >> 10) == pre) atomicAdd(&hist[col][key & 1023u], 1u);
+      else if ((key >> 10) > pre) above = min(above, key);
+    }
+    atomicMin(&above_s[col], above);
+  }
+  __syncthreads();
+  find_rank(hist, 1024, k_s, part, bin_s, rank_s);
+  __syncthreads();
+  const uint32_t d3 = bin_s[col] & 1023u;
+  const uint32_t lo = (pre << 10) | d3;
+  // the upper middle value of an even count: lo again if its bin holds the
+  // next rank too, else the next non-empty bin above it, else the smallest
+  // key above the prefix
+  const bool same = rank_s[col] + 1 < int64_t(hist[col][d3]);
+  {
+    const int run = 1024 / kStatGroups;
+    uint32_t nb = 0xFFFFFFFFu;
+    for (int bb = grp * run; bb < (grp + 1) * run; ++bb)
+      if (uint32_t(bb) > d3 && hist[col][bb] != 0u) { nb = uint32_t(bb); break; }
+    if (nb != 0xFFFFFFFFu) atomicMin(&next_s[col], nb);
+  }
+  __syncthreads();
+  if (grp == 0 && live) {
+    uint32_t hi = lo;
+    if (nrows % 2 == 0 && !same)
+      hi = next_s[col] != 0xFFFFFFFFu ? ((pre << 10) | next_s[col]) : above_s[col];
     maxabs[c] = double(__uint_as_float(mx_s[col]));
     // the mean of the two middle values for an even count, as a median of an
     // even number of values is usually defined
@@ -196,8 +262,55 @@ expect_silu_sq_kernel(const double* __restrict__ var, int64_t n, GaussHermite gh
   out[i] = scale ? e * scale[i] : e;
 }
 
-// out[r][j] = in[r][perm[j]] (gather) or out[r][perm[j]] = in[r][j] (scatter);
-// grid-stride over the elements.
+// out[r][j] = in[r][perm[j]] (gather) or out[r][perm[j]] = in[r][j] (scatter).
+// Rows of up to kPermLdsCols columns go through LDS: a workgroup reads a whole
+// row with coalesced loads into LDS (in place for the gather, at perm[j] for
+// the scatter), then writes the whole output row with coalesced stores (from
+// perm[j] for the gather, in place for the scatter), so both HBM sides stream.
+// For the scatter a bit per column marks the positions some valid entry
+// targets; the others are left unwritten, as in the direct form. Wider rows
+// take the direct form: one thread per element, grid-stride.
+constexpr int64_t kPermLdsCols = 16384;   // 64 KB of row plus 2 KB of marks
+
+__global__ void __launch_bounds__(kThreads)
+permute_rows_lds_kernel(const float* __restrict__ in, int64_t nrows, int64_t ncols,
+                        const int32_t* __restrict__ perm, int inverse, float* __restrict__ out) {
+  extern __shared__ uint32_t perm_lds[];
+  float* row = reinterpret_cast<float*>(perm_lds);
+  uint32_t* mark = perm_lds + ncols;   // (ncols + 31) / 32 words, scatter only
+  const int n = int(ncols);
+  if (inverse) {
+    for (int w = threadIdx.x; w < (n + 31) / 32; w += kThreads) mark[w] = 0u;
+    __syncthreads();
+    for (int j = threadIdx.x; j < n; j += kThreads) {
+      const int32_t p = perm[j];
+      if (p >= 0 && p < n) atomicOr(&mark[p / 32], 1u << (p % 32));
+    }
+  }
+  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    __syncthreads();   // the previous row's reads of the buffer are done
+    const float* src = in + r * ncols;
+    float* dst = out + r * ncols;
+    for (int j = threadIdx.x; j < n; j += kThreads) {
+      if (!inverse) {
+        row[j] = src[j];
+      } else {
+        const int32_t p = perm[j];
+        if (p >= 0 && p < n) row[p] = src[j];
+      }
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < n; j += kThreads) {
+      if (!inverse) {
+        const int32_t p = perm[j];
+        dst[j] = (p >= 0 && p < n) ? row[p] : __int_as_float(0x7fc00000);
+      } else if ((mark[j / 32] >> (j % 32)) & 1u) {
+        dst[j] = row[j];
+      }
+    }
+  }
+}
+
 __global__ void __launch_bounds__(kThreads)
 permute_columns_kernel(const float* __restrict__ in, int64_t nrows, int64_t ncols,
                        const int32_t* __restrict__ perm, int inverse, float* __restrict__ out) {
@@ -265,7 +378,8 @@ hipError_t launch_sq_gemv(const float* d_W, int64_t nrows, int64_t ncols, const 
 
 hipError_t launch_column_stats(const float* d_W, int64_t nrows, int64_t ncols, double* d_max,
                                double* d_median, hipStream_t stream) {
-  const unsigned grid = unsigned((ncols + kStatCols - 1) / kStatCols);
+  const int64_t groups = (ncols + kStatCols - 1) / kStatCols;
+  const unsigned grid = unsigned((groups + kStatSuper - 1) / kStatSuper * kStatSuper);
   hipLaunchKernelGGL(column_stats_kernel, dim3(grid), dim3(kThreads), 0, stream, d_W, nrows, ncols,
                      d_max, d_median);
   return hipGetLastError();
@@ -332,6 +446,18 @@ hipError_t launch_propagate_down(const float* d_Wgate, const float* d_Wup, int64
 hipError_t launch_permute_columns(const float* d_in, int64_t nrows, int64_t ncols,
                                   const int32_t* d_perm, int inverse, float* d_out,
                                   hipStream_t stream) {
+  if (ncols <= kPermLdsCols) {
+    const size_t lds = size_t(ncols) * 4 + size_t((ncols + 31) / 32) * 4;
+    // more than 64 KB of dynamic LDS must be allowed for the kernel once
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(permute_rows_lds_kernel),
+        hipFuncAttributeMaxDynamicSharedMemorySize, int(kPermLdsCols * 4 + kPermLdsCols / 8));
+    if (attr != hipSuccess) return attr;
+    const int64_t blocks = std::min<int64_t>(nrows, 8192);
+    hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(unsigned(blocks)), dim3(kThreads), lds, stream,
+                       d_in, nrows, ncols, d_perm, inverse, d_out);
+    return hipGetLastError();
+  }
   const int64_t blocks = std::min<int64_t>((nrows * ncols + kThreads - 1) / kThreads, 65536);
   hipLaunchKernelGGL(permute_columns_kernel, dim3(unsigned(blocks)), dim3(kThreads), 0, stream, d_in,
                      nrows, ncols, d_perm, inverse, d_out);

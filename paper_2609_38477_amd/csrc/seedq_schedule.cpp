@@ -20,6 +20,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <thread>
 #include <vector>
 
 #include "seedq_internal.h"
@@ -33,12 +34,126 @@ struct Breakpoint {
   int step;  // hull step j (promotion from position j to j + 1)
 };
 
+// The sweep's order: larger lambda first, then the lower class, then the
+// lower step.
+bool before(const Breakpoint& a, const Breakpoint& b) {
+  if (a.lam != b.lam) return a.lam > b.lam;
+  if (a.cls != b.cls) return a.cls < b.cls;
+  return a.step < b.step;
+}
+
+// Runs f(t, begin, end) on nt threads over [0, n) in contiguous chunks (the
+// planner's large-input loops; every chunk's work is independent, so the
+// result does not depend on the thread count).
+template <typename F>
+void parallel_chunks(int64_t n, int nt, F&& f) {
+  if (nt <= 1 || n < 2 * nt) {
+    f(0, int64_t(0), n);
+    return;
+  }
+  std::vector<std::thread> th;
+  th.reserve(size_t(nt - 1));
+  for (int t = 1; t < nt; ++t)
+    th.emplace_back([&, t] { f(t, n * t / nt, n * (t + 1) / nt); });
+  f(0, int64_t(0), n / nt);
+  for (auto& x : th) x.join();
+}
+
+int planner_threads(int64_t n) {
+  if (n < (int64_t(1) << 18)) return 1;
+  const unsigned hc = std::thread::hardware_concurrency();
+  return int(std::max(1u, std::min(hc, 16u)));
+}
+
+// Indices 0..n-1 ordered by v ascending, equal values by index (and the values
+// in that order, in sorted_v). Large inputs take a stable LSD radix sort on the
+// bit patterns of v (the values are positive and finite, so their bits order
+// like them), 11 bits per pass (a bucket table that stays in cache), passes
+// whose digit every key shares skipped, each pass split over threads (per-thread
+// counts, offsets in thread order, so the scatter stays stable); small inputs
+// std::sort.
+std::vector<int64_t> order_by_value(const std::vector<double>& v, std::vector<double>& sorted_v) {
+  const int64_t n = int64_t(v.size());
+  std::vector<int64_t> idx(n);
+  sorted_v.resize(size_t(n));
+  if (n < (int64_t(1) << 16)) {
+    for (int64_t i = 0; i < n; ++i) idx[i] = i;
+    std::sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
+      return v[a] < v[b] || (v[a] == v[b] && a < b);
+    });
+    for (int64_t k = 0; k < n; ++k) sorted_v[k] = v[idx[k]];
+    return idx;
+  }
+  const int nt = planner_threads(n);
+  std::vector<uint64_t> key(n), key2(n);
+  std::vector<int64_t> idx2(n);
+  parallel_chunks(n, nt, [&](int, int64_t b, int64_t e) {
+    for (int64_t i = b; i < e; ++i) {
+      std::memcpy(&key[i], &v[i], sizeof(double));
+      idx[i] = i;
+    }
+  });
+  constexpr int kBits = 11, kBuckets = 1 << kBits;
+  constexpr uint64_t kMask = kBuckets - 1;
+  std::vector<int64_t> cnt(size_t(nt) * kBuckets);
+  for (int shift = 0; shift < 64; shift += kBits) {
+    std::fill(cnt.begin(), cnt.end(), 0);
+    parallel_chunks(n, nt, [&](int t, int64_t b, int64_t e) {
+      int64_t* c = cnt.data() + size_t(t) * kBuckets;
+      for (int64_t i = b; i < e; ++i) ++c[(key[i] >> shift) & kMask];
+    });
+    const uint64_t d0 = (key[0] >> shift) & kMask;
+    int64_t same = 0;
+    for (int t = 0; t < nt; ++t) same += cnt[size_t(t) * kBuckets + d0];
+    if (same == n) continue;   // one digit for all
+    int64_t run = 0;
+    for (int d = 0; d < kBuckets; ++d)
+      for (int t = 0; t < nt; ++t) {
+        int64_t& c = cnt[size_t(t) * kBuckets + d];
+        const int64_t x = c;
+        c = run;
+        run += x;
+      }
+    parallel_chunks(n, nt, [&](int t, int64_t b, int64_t e) {
+      int64_t* c = cnt.data() + size_t(t) * kBuckets;
+      for (int64_t i = b; i < e; ++i) {
+        const int64_t pos = c[(key[i] >> shift) & kMask]++;
+        key2[pos] = key[i];
+        idx2[pos] = idx[i];
+      }
+    });
+    key.swap(key2);
+    idx.swap(idx2);
+  }
+  std::memcpy(sorted_v.data(), key.data(), sizeof(double) * size_t(n));
+  return idx;
+}
+
+// The neighbouring doubles of a non-negative finite x: for these the bit
+// pattern counts the representable values (std::nextafter's result, without
+// the library call).
+double next_up(double x) {
+  uint64_t b;
+  std::memcpy(&b, &x, sizeof b);
+  ++b;
+  std::memcpy(&x, &b, sizeof b);
+  return x;
+}
+double next_down(double x) {   // x > 0
+  uint64_t b;
+  std::memcpy(&b, &x, sizeof b);
+  --b;
+  std::memcpy(&x, &b, sizeof b);
+  return x;
+}
+
 // Largest lambda >= 0 with fl(lambda / s) <= v (v > 0, s > 0).
 double breakpoint(double v, double s) {
   double lam = v * s;
-  while (lam > 0.0 && lam / s > v) lam = std::nextafter(lam, 0.0);
+  if (!std::isfinite(lam)) lam = std::nextafter(INFINITY, 0.0);
+  while (lam > 0.0 && lam / s > v) lam = next_down(lam);
   for (;;) {
-    const double up = std::nextafter(lam, INFINITY);
+    const double up = next_up(lam);
     if (std::isfinite(up) && up / s <= v) lam = up;
     else break;
   }
@@ -173,7 +288,10 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
     qf = 1.0 * sg[kq / nrows];
   } else {
     std::vector<double> all(nb);
-    for (int64_t b = 0; b < nb; ++b) all[b] = imp_of(b);
+    parallel_chunks(nrows, planner_threads(nb), [&](int, int64_t r0, int64_t r1) {
+      for (int64_t r = r0; r < r1; ++r)
+        for (int64_t g = 0; g < G; ++g) all[r * G + g] = rho[r] * abar[g];   // = imp_of(r G + g)
+    });
     std::nth_element(all.begin(), all.begin() + kq, all.end());
     qf = all[kq];
   }
@@ -185,24 +303,33 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
   std::vector<int32_t> cls_of;  // per group (rho == 1) or per block
   {
     const int64_t n = rho.empty() ? G : nb;
-    std::vector<int64_t> idx(n);
-    for (int64_t i = 0; i < n; ++i) idx[i] = i;
     auto val = [&](int64_t i) { return std::max(rho.empty() ? 1.0 * abar[i] : imp_of(i), qf); };
     std::vector<double> v(n);
-    for (int64_t i = 0; i < n; ++i) v[i] = val(i);
-    std::sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
-      return v[a] < v[b] || (v[a] == v[b] && a < b);
-    });
-    cls_of.assign(n, -1);
+    if (rho.empty()) {
+      for (int64_t i = 0; i < n; ++i) v[i] = val(i);
+    } else {
+      parallel_chunks(nrows, planner_threads(n), [&](int, int64_t r0, int64_t r1) {
+        for (int64_t r = r0; r < r1; ++r)
+          for (int64_t g = 0; g < G; ++g) v[r * G + g] = std::max(rho[r] * abar[g], qf);   // = val(r G + g)
+      });
+    }
+    std::vector<double> sv;
+    const std::vector<int64_t> idx = order_by_value(v, sv);
+    // class of every rank (a new class where the value changes), then the
+    // scatter to block order
+    std::vector<int32_t> cls_at(static_cast<size_t>(n));
     for (int64_t k = 0; k < n; ++k) {
-      const int64_t i = idx[k];
-      if (cls_val.empty() || v[i] != cls_val.back()) {
-        cls_val.push_back(v[i]);
+      if (cls_val.empty() || sv[k] != cls_val.back()) {
+        cls_val.push_back(sv[k]);
         cls_count.push_back(0);
       }
-      cls_of[i] = int32_t(cls_val.size() - 1);
+      cls_at[k] = int32_t(cls_val.size() - 1);
       cls_count.back() += rho.empty() ? nrows : 1;
     }
+    cls_of.assign(n, -1);
+    parallel_chunks(n, planner_threads(n), [&](int, int64_t k0, int64_t k1) {
+      for (int64_t k = k0; k < k1; ++k) cls_of[idx[k]] = cls_at[k];
+    });
   }
   const int ncls = int(cls_val.size());
 
@@ -213,16 +340,41 @@ int plan_schedule(const seedq_schedule_desc* d, uint8_t* rob, seedq_schedule_rep
   if (double(nb) * bits[H[0]] > double(budget)) return SEEDQ_ERATE;
 
   // ---- breakpoint sweep
+  // For one step the breakpoint grows with the class value, and the classes
+  // are numbered by increasing value: each step's list comes out in sweep
+  // order by walking the classes downwards (equal breakpoints of neighbouring
+  // classes put back in class order), and the lists are merged.
   std::vector<int> level(ncls, 0);
   std::vector<Breakpoint> ev;
   ev.reserve(size_t(ncls) * (J > 1 ? J - 1 : 0));
-  for (int c = 0; c < ncls; ++c)
-    for (int j = 0; j + 1 < J; ++j) ev.push_back({breakpoint(cls_val[c], slope[j]), c, j});
-  std::sort(ev.begin(), ev.end(), [](const Breakpoint& a, const Breakpoint& b) {
-    if (a.lam != b.lam) return a.lam > b.lam;
-    if (a.cls != b.cls) return a.cls < b.cls;
-    return a.step < b.step;
-  });
+  {
+    std::vector<std::vector<Breakpoint>> lists(J > 1 ? J - 1 : 0);
+    for (int j = 0; j + 1 < J; ++j) {
+      std::vector<Breakpoint>& L = lists[j];
+      L.resize(size_t(ncls));
+      parallel_chunks(ncls, planner_threads(ncls), [&](int, int64_t b, int64_t e) {
+        for (int64_t i = b; i < e; ++i) {
+          const int c = ncls - 1 - int(i);
+          L[size_t(i)] = {breakpoint(cls_val[c], slope[j]), c, j};
+        }
+      });
+      for (size_t a = 0; a < L.size();) {
+        size_t b = a + 1;
+        while (b < L.size() && L[b].lam == L[a].lam) ++b;
+        std::reverse(L.begin() + long(a), L.begin() + long(b));
+        a = b;
+      }
+    }
+    std::vector<size_t> at(lists.size(), 0);
+    for (;;) {
+      int best = -1;
+      for (int j = 0; j < int(lists.size()); ++j)
+        if (at[j] < lists[j].size() && (best < 0 || before(lists[j][at[j]], lists[best][at[best]])))
+          best = j;
+      if (best < 0) break;
+      ev.push_back(lists[best][at[best]++]);
+    }
+  }
 
   int64_t total = nb * int64_t(bits[H[0]]);
   double lam = 0.0;

@@ -97,3 +97,24 @@ def test_derive_errors(sq):
     with pytest.raises(sq.SeedqError) as e:
         sq.derive_schedule(4, 64, RUNGS, None, a, rep["lam"], rep["floor_q"], 0)
     assert e.value.code == -4
+
+
+@pytest.mark.parametrize("case", ["random", "tied"])
+def test_planner_large_with_rows_matches_oracle(sq, oq, case):
+    """Above 2^18 blocks the planner sorts its importance classes with a
+    threaded radix sort and merges per-step breakpoint lists: the allocation,
+    lambda and tie count must still be the oracle's."""
+    rng = np.random.default_rng(11 if case == "random" else 12)
+    nrows, ncols = 600, 4096
+    a = np.exp(rng.normal(0, 1, ncols)).astype(np.float32)
+    rho = np.exp(rng.normal(0, 0.5, nrows)).astype(np.float32)
+    if case == "tied":      # few distinct factors: large classes of equal importance
+        a = np.round(a * 2).clip(1).astype(np.float32)
+        rho = np.round(rho * 2).clip(1).astype(np.float32)
+    target = 3.9 if case == "random" else 4.05
+    enc, rep = sq.plan_schedule(nrows, ncols, RUNGS, DAMAGE, target, a, rho, 0.06)
+    ref = oq.schedule(nrows, ncols, RUNGS, DAMAGE, target, a, rho, 0.06)
+    assert rep["lam"] == ref.lam and rep["tie_count"] == ref.tie_count
+    assert np.array_equal(enc, ref.rung_of_block)
+    if case == "tied":
+        assert rep["tie_count"] > 0

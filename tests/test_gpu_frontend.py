@@ -53,6 +53,24 @@ def test_column_stats_exact(sq, nrows):
     assert np.array_equal(mx.cpu().numpy(), rmx) and np.array_equal(md.cpu().numpy(), rmd)
 
 
+@pytest.mark.parametrize("shape", [(1000, 600), (3, 257), (4096, 264)])
+def test_column_stats_exact_many_columns(sq, shape):
+    """Column groups spread over several workgroup super-blocks (and a ragged
+    last one), heavy ties in low bits, values straddling digit boundaries."""
+    import torch
+    nrows, ncols = shape
+    rng = np.random.default_rng(ncols)
+    W = rng.normal(0, 0.02, shape).astype(np.float32)
+    W[:, 1] = np.float32(1.0) + np.float32(2 ** -23) * rng.integers(0, 4, nrows)   # last-digit ties
+    W[:, 2] = np.ldexp(np.float32(1), rng.integers(-30, 30, nrows)).astype(np.float32)
+    W[: nrows // 2, ncols - 1] = 0.0
+    mx = torch.empty(ncols, dtype=torch.float64, device="cuda")
+    md = torch.empty_like(mx)
+    sq.seedq_column_stats(_t(W), nrows, ncols, mx, md)
+    rmx, rmd = oimp.column_stats(W)
+    assert np.array_equal(mx.cpu().numpy(), rmx) and np.array_equal(md.cpu().numpy(), rmd)
+
+
 def test_expect_silu_sq_matches_oracle(sq):
     import torch
     var = np.concatenate([[0.0, 1e-8], np.geomspace(1e-4, 16, 200)])
