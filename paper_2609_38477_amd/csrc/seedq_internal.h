@@ -60,7 +60,9 @@ __host__ __device__ constexpr int pair_index(int i, int j) { return i * kC - i *
 // projection gives the least-squares residual without cancellation.
 constexpr int kComplementMinP = 5;
 __host__ __device__ constexpr int complement_dims(int P) { return P >= kComplementMinP ? kC - P : 0; }
-constexpr float kComplementScale = 256.0f;      // 2^8 on the complement operand
+// 2^4 on the complement operand: the squared projections of a block scaled to
+// max |w_i| in [1, 2) stay below 2^13, inside fp16's range (the P = 6 records)
+constexpr float kComplementScale = 16.0f;
 
 // Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
 //   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
@@ -77,7 +79,7 @@ constexpr float kComplementScale = 256.0f;      // 2^8 on the complement operand
 //   nc16:   fp16 [ntiles][M][64][8], M = complement_dims(P) (empty below
 //           kComplementMinP): MFMA A fragments of the complement basis n_c of
 //           range(U(s)), c < M; fragment c of tile T, lane l, element e is
-//           hi(2^8 n_c[e]) for l < 32 and lo(2^8 n_c[e]) = fp16(2^8 n_c[e] -
+//           hi(2^4 n_c[e]) for l < 32 and lo(2^4 n_c[e]) = fp16(2^4 n_c[e] -
 //           hi) for l >= 32, of seed 32T + (l % 32) + 1 (zero beyond 2^K - 1)
 // Widest LFSR whose centred states fit int16 (|x - 2^(K-1)| <= 2^(K-1)).
 constexpr int kPackedMaxK = 16;

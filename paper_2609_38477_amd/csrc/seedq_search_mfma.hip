@@ -197,9 +197,9 @@ SEEDQ_INLINE floatx16 bounds(const half8& a0, const half8& a1, const half8& a2, 
   return acc;
 }
 
-// Complement screen (P >= kComplementMinP): the projections d_c = 2^8 n_c^T w
+// Complement screen (P >= kComplementMinP): the projections d_c = 2^4 n_c^T w
 // of a block on the M complement vectors of 32 seeds are M products with K =
-// 16 (the hi and lo parts of 2^8 n_c against the block's fp16 weights, given
+// 16 (the hi and lo parts of 2^4 n_c against the block's fp16 weights, given
 // twice), and -sum_c d_c^2 is returned so that the max-fold, the records and
 // the pilot treat it like the quadratic form's bound: larger passes.
 template <int M>
@@ -297,13 +297,12 @@ constexpr int kQCapRec = 64 + 64 * 16;        // < 64 waiting + one round of 64 
 // 2 bytes: two float4 of storage instead of four), which brings the kernel's
 // LDS to 40 KB and, with at most 128 VGPRs, four waves per SIMD (measured on
 // 2.1 M blocks: (14..16,6) 5-6 % faster; at P = 5 the register limit spills
-// and measured 18 % slower). The values -sum d^2 are scaled by 2^-8 into fp16
-// range (|d| < 2^11) and rounded toward zero, i.e. up, so that a stored bound
-// is never below the computed one.
+// and measured 18 % slower). The values -sum d^2 lie in fp16's range (|sum
+// d^2| < 2^13 with the complement operand's 2^4 scale) and are rounded toward
+// zero, i.e. up, so that a stored bound is never below the computed one.
 __host__ __device__ constexpr bool half_records(int P) { return complement_dims(P) == 2; }
 template <int P>
 constexpr int kRecVecs = half_records(P) ? 2 : 4;
-constexpr float kRecScale = 0x1p-8f;
 typedef __fp16 fp16x2 __attribute__((ext_vector_type(2)));
 
 template <int P>
@@ -401,8 +400,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
         // sqrt(M) times the bound on the error of each computed projection,
         // in accumulator units (kComplementScale): fp16 rounding of the
         // weights (2^-11 relative each, Cauchy-Schwarz with |n_c| = 1) plus
-        // that of the hi/lo complement vector (2^-22 relative, 2^-25 for
-        // subnormal parts) and the fp32 accumulation of 16 exact products,
+        // that of the hi/lo complement vector (2^-22 relative; below fp16's
+        // normal range 2^-25 absolute in the 2^4-scaled entries, 2^-29 of
+        // n_c) and the fp32 accumulation of 16 exact products,
         // all under 2^-11 (1 + 2^-7) |w| + 2^-20; |w| <= sqrt(ww) (1 + 2^-20)
         const float norm = sqrtf(ww) * (1.0f + 0x1p-20f);
         slot_thr[nt * 32 + n] = sqrtf(float(M)) * (1.0f + 0x1p-20f) * kComplementScale *
@@ -424,9 +424,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     if (key == ~0ull) return -INFINITY;
     if constexpr (M > 0) {
       // a seed whose residual r_LS(w) is at most the best error b has computed
-      // projections of norm <= 2^8 sqrt(b 2^-2ex) + slot_thr (triangle
+      // projections of norm <= 2^4 sqrt(b 2^-2ex) + slot_thr (triangle
       // inequality over the M of them), so their fp32 sum of squares (within
-      // 2^-20 of its value) is at most T = (2^8 sqrt(b 2^-2ex) + slot_thr)^2
+      // 2^-20 of its value) is at most T = (2^4 sqrt(b 2^-2ex) + slot_thr)^2
       // (1 + 2^-19). Evaluated in fp32 and rounded up by the factors below:
       // the nearest-rounded conversion (2^-24 relative, 2^-150 absolute below
       // the normal range), sqrtf (1 ulp) and each later rounding (2^-24).
@@ -512,9 +512,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
         float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0;
         if (live) {
           m = meta[base + lane];
-          // the stored bounds are scaled by 2^-8; so is the threshold, less
-          // 2^-140 for the rounding of the scaling below the normal range
-          t = fmaf(slot_threshold(int(m & 0x7Fu)), kRecScale, -0x1p-140f);
+          t = slot_threshold(int(m & 0x7Fu));
           r0 = rec[base + lane][0];
           r1 = rec[base + lane][1];
         }
@@ -606,8 +604,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
         float pk[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k)
-          pk[k] = __builtin_bit_cast(float, __builtin_amdgcn_cvt_pkrtz(acc[2 * k] * kRecScale,
-                                                                       acc[2 * k + 1] * kRecScale));
+          pk[k] = __builtin_bit_cast(float, __builtin_amdgcn_cvt_pkrtz(acc[2 * k], acc[2 * k + 1]));
         rec[r][0] = make_float4(pk[0], pk[1], pk[2], pk[3]);
         rec[r][1] = make_float4(pk[4], pk[5], pk[6], pk[7]);
       } else {
