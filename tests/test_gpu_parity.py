@@ -343,16 +343,45 @@ def test_search_k20_sampled(sq, oq, torch):
 
 @pytest.mark.parametrize("K,P,nb", [(16, 6, 48), (15, 6, 64), (16, 5, 48)])
 def test_search_dense_survivor_rungs(sq, oq, torch, K, P, nb):
-    # rungs where a few percent of all seeds pass the matrix core's screen: the
-    # lane-mask enqueue (P >= 5) and, at P = 6 and K >= 15, the fp32 residual
-    # filter in front of the exact evaluation; 48 or 64 blocks leave part of a
-    # wave's four 32-block tiles empty; heavy-tailed blocks among them
+    # rungs where a few percent of all seeds pass the screen: the complement
+    # screen and its records (fp16 at P = 6), the integer basis table in the
+    # exact evaluation; 48 or 64 blocks leave part of a wave's four 32-block
+    # tiles empty; heavy-tailed blocks among them
     W = synthetic.weights(1, 8 * nb, 0.02, key=60 + K + P, outlier_frac=0.05)
     b = sq.build_bases(K, P)
     seed, e, q, err = sq.compress(_dev(torch, W), [b])
     torch.cuda.synchronize()
     check_search(oq, W, K, P, seed.cpu().numpy().view(np.uint32), e.cpu().numpy(),
                  q.cpu().numpy(), err.cpu().numpy(), f"K{K}P{P}")
+
+
+@pytest.mark.parametrize("K,P", [(11, 5), (11, 6), (13, 6)])
+def test_search_rank_deficient_seeds_complement(sq, oq, torch, K, P):
+    # blocks in (or next to) the column span of the rank-deficient seeds of a
+    # P >= 5 rung: their residual at that seed is zero, so the seed must
+    # survive the complement screen, whose vectors span only part of that
+    # seed's larger complement, and the refine takes the minimum-norm solution
+    U = oq.basis_int_all(K, P).astype(np.float64) * 2.0 ** -(K - 1)
+    s = np.linalg.svd(U, compute_uv=False)
+    deficient = np.nonzero(s[:, -1] <= 2.0 ** -30 * s[:, 0])[0]
+    assert len(deficient) > 0
+    rng = np.random.default_rng(K * 8 + P)
+    blocks = []
+    for idx in deficient:
+        for k in range(8):
+            w = U[idx] @ rng.normal(0, 0.05, P)
+            if k >= 4:
+                w = w + rng.normal(0, 1e-4, 8)
+            blocks.append(w)
+    W = np.asarray(blocks, dtype=np.float32).reshape(1, -1)
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(_dev(torch, W), [b])
+    torch.cuda.synchronize()
+    seed = seed.cpu().numpy().view(np.uint32)
+    ref = check_search(oq, W, K, P, seed, e.cpu().numpy(), q.cpu().numpy(), err.cpu().numpy(),
+                       f"K{K}P{P} rank-deficient")
+    # the searches did land on those seeds for some blocks (the case is live)
+    assert np.isin(ref.seed, deficient + 1).any()
 
 
 def test_search_full_size_attention_sampled(sq, oq, torch):
