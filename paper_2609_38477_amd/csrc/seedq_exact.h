@@ -49,9 +49,15 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
     q[p] = int(r);
   }
   // acc_i = sum_j u[j][i] q_j, exact in int32 (|u| < 2^23, |q| <= 8, P <= 6).
-  // From the table the basis address is made to depend on e, so that its loads
-  // are issued after the coefficient loads are consumed and the two sets of
-  // registers are not live at once.
+  // From the table the basis address is made to depend on e (a zero offset
+  // the compiler cannot see through), so that its loads are issued after the
+  // coefficient loads are consumed and the two sets of registers are not live
+  // at once; the pointer itself keeps its global address space.
+  auto after = [](int dep) {
+    uint32_t z = 0u;
+    asm volatile("" : "+v"(z) : "v"(dep));
+    return z;
+  };
   int32_t acc[kC];
   if constexpr (!kTable) {
     // the states by LFSR steps from the seed: fewer registers than the table
@@ -69,10 +75,9 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
       }
     }
   } else if (K <= kPackedMaxK) {
-    asm volatile("" : "+v"(Ub) : "v"(e));
     // two coefficients per dot2 (v_dot2_i32_i16)
     constexpr int PW = (P + 1) / 2;
-    const uint4* src = reinterpret_cast<const uint4*>(Ub);
+    const uint4* src = reinterpret_cast<const uint4*>(Ub) + after(e);
 #pragma unroll
     for (int i = 0; i < kC; ++i) acc[i] = 0;
 #pragma unroll
@@ -87,8 +92,7 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
         acc[i] = __builtin_amdgcn_sdot2(__builtin_bit_cast(seedq_short2, u[i]), qv, acc[i], false);
     }
   } else {
-    asm volatile("" : "+v"(Ub) : "v"(e));
-    const uint4* src = reinterpret_cast<const uint4*>(Ub);
+    const uint4* src = reinterpret_cast<const uint4*>(Ub) + after(e);
 #pragma unroll
     for (int i = 0; i < kC; ++i) acc[i] = 0;
 #pragma unroll

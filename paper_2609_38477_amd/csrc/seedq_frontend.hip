@@ -448,8 +448,9 @@ hipError_t launch_permute_columns(const float* d_in, int64_t nrows, int64_t ncol
                                   hipStream_t stream) {
   if (ncols <= kPermLdsCols) {
     const size_t lds = size_t(ncols) * 4 + size_t((ncols + 31) / 32) * 4;
-    // more than 64 KB of dynamic LDS must be allowed for the kernel once
-    static const hipError_t attr = hipFuncSetAttribute(
+    // more than 64 KB of dynamic LDS must be allowed for the kernel (set on
+    // every call: the attribute belongs to the current device)
+    const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(permute_rows_lds_kernel),
         hipFuncAttributeMaxDynamicSharedMemorySize, int(kPermLdsCols * 4 + kPermLdsCols / 8));
     if (attr != hipSuccess) return attr;
