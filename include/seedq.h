@@ -152,8 +152,10 @@ int seedq_bases_bytes(int32_t K, int32_t P, int32_t C, size_t* bytes);
 /*
  * LFSR basis generation and per-seed pseudo-inverses for every seed of a rung
  * (section 3.1: U(s) from the LFSR started at s; the least-squares fit needs
- * pinv(U(s))). Integer LFSR stepping is bit-exact; the pseudo-inverse and the
- * orthonormal range basis come from a one-sided Jacobi SVD in fp64.
+ * pinv(U(s))). Integer LFSR stepping is bit-exact and the states are kept as
+ * each seed's integer basis; the pseudo-inverse, the projector onto range(U(s))
+ * and (for P >= 5) orthonormal vectors of its complement come from a one-sided
+ * Jacobi SVD in fp64.
  *   d_bases: device buffer of seedq_bases_bytes(K, P, C) bytes, 256-byte aligned.
  *   d_U:     optional (NULL to skip) device int32 [2^K - 1][P][8]: U_int(s) for
  *            s = 1 .. 2^K-1 (row s-1; element [j][i] = centred state x_{8j+i}).
