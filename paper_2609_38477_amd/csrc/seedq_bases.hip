@@ -45,7 +45,8 @@ build_bases_kernel(int K, uint32_t mask, int64_t nseeds, double* __restrict__ pi
   if (idx >= nseeds) {
     // padding seeds of the last tile
     if (tile * kSeedTile < nseeds) {
-      for (int k = 0; k < kPairsPadded; ++k) *pi_at(k) = _Float16(0.0f);
+      if constexpr (M == 0)
+        for (int k = 0; k < kPairsPadded; ++k) *pi_at(k) = _Float16(0.0f);
       for (int c = 0; c < M; ++c)
         for (int e = 0; e < kC; ++e) *nc_at(c, 0, e) = *nc_at(c, 1, e) = _Float16(0.0f);
     }
@@ -138,23 +139,26 @@ build_bases_kernel(int K, uint32_t mask, int64_t nseeds, double* __restrict__ pi
   }
 
   // projector Pi = sum over kept j of u_j u_j^T, 2^12-scaled fp16 fragments
+  // (P <= 4; P >= 5 screens with the complement vectors below instead)
   {
     double Un[kC][P];
 #pragma unroll
     for (int i = 0; i < kC; ++i)
 #pragma unroll
       for (int j = 0; j < P; ++j) Un[i][j] = A[i][j] * inv1[j];
+    if constexpr (M == 0) {
 #pragma unroll
-    for (int i = 0; i < kC; ++i) {
+      for (int i = 0; i < kC; ++i) {
 #pragma unroll
-      for (int j2 = i; j2 < kC; ++j2) {
-        double v = 0.0;
+        for (int j2 = i; j2 < kC; ++j2) {
+          double v = 0.0;
 #pragma unroll
-        for (int j = 0; j < P; ++j) v = fma(Un[i][j], Un[j2][j], v);
-        *pi_at(pair_index(i, j2)) = _Float16(float(v * double(kOperandScale)));
+          for (int j = 0; j < P; ++j) v = fma(Un[i][j], Un[j2][j], v);
+          *pi_at(pair_index(i, j2)) = _Float16(float(v * double(kOperandScale)));
+        }
       }
+      for (int k = kPairs; k < kPairsPadded; ++k) *pi_at(k) = _Float16(0.0f);
     }
-    for (int k = kPairs; k < kPairsPadded; ++k) *pi_at(k) = _Float16(0.0f);
 
     if constexpr (M > 0) {
       double N[M][kC];

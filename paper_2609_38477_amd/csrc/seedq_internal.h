@@ -72,7 +72,8 @@ constexpr float kComplementScale = 16.0f;
 //           << 16, zero high half past P), above it int32 (word j*8 + i =
 //           u[j][i]); the exact evaluation reads it instead of stepping the
 //           LFSR
-//   pi16:   fp16 [ntiles][3][64][8]  2^12 Pi_s[k] as MFMA A-operand fragments:
+//   pi16:   fp16 [ntiles][3][64][8] (empty from kComplementMinP on) 2^12 Pi_s[k]
+//           as MFMA A-operand fragments:
 //           tile T holds seeds 32T+1 .. 32T+32; fragment t, lane l, element e
 //           is pair k = 16t + 8(l/32) + e of seed 32T + (l%32) + 1 (zero for
 //           k >= 36 and for seeds beyond 2^K - 1)
@@ -101,7 +102,7 @@ inline BasesLayout bases_layout(int K, int P) {
   L.off_pinv64 = 0;
   L.off_ub = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
   L.off_pi16 = align256(L.off_ub + size_t(L.nseeds) * basis_words(K, P) * sizeof(uint32_t));
-  L.off_nc16 = align256(L.off_pi16 + size_t(L.ntiles) * kTileBytes);
+  L.off_nc16 = align256(L.off_pi16 + (complement_dims(P) > 0 ? 0 : size_t(L.ntiles) * kTileBytes));
   L.total = align256(L.off_nc16 + size_t(L.ntiles) * complement_dims(P) * 64 * kC * 2);
   return L;
 }
