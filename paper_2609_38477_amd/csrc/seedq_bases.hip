@@ -67,12 +67,11 @@ build_bases_kernel(int K, uint32_t mask, int64_t nseeds, double* __restrict__ pi
       const int32_t u = int32_t(x) - half;
       if (U_out) U_out[idx * (P * kC) + j * kC + i] = u;
       A[i][j] = double(u) * scale;
-      if (!packed) {
-        Ub[j * kC + i] = uint32_t(u);
-      } else if (j % 2 == 0) {
-        Ub[(j / 2) * kC + i] = uint32_t(uint16_t(int16_t(u)));   // high half below
-      } else {
-        Ub[(j / 2) * kC + i] |= uint32_t(uint16_t(int16_t(u))) << 16;
+      if (packed) {   // no table above kPackedMaxK
+        if (j % 2 == 0)
+          Ub[(j / 2) * kC + i] = uint32_t(uint16_t(int16_t(u)));   // high half below
+        else
+          Ub[(j / 2) * kC + i] |= uint32_t(uint16_t(int16_t(u))) << 16;
       }
       x = lfsr_step(x, mask);
     }

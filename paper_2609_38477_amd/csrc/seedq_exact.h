@@ -10,11 +10,11 @@ typedef short seedq_short2 __attribute__((ext_vector_type(2)));
 
 // Quantised error of seed s for block w (fp64, exact reconstruction).
 // A:  pinv(U(s)), P x 8 row-major (fp64).
-// kTable: read the states from the table Ub, else step the LFSR (mask) from s.
-// Ub: the seed's integer basis from the basis stack (see BasesLayout): for
-//     K <= kPackedMaxK, (P+1)/2 x 8 words, word (j, i) = the centred states
-//     u[2j][i] (low half) and u[2j+1][i] (high half) as int16; above it, P x 8
-//     int32 words u[j][i]. u[j][i] = x_{8j+i} - 2^(K-1), x_0 = s.
+// kTable and K <= kPackedMaxK: read the states from the table Ub, else step
+// the LFSR (mask) from s. Ub: the seed's integer basis from the basis stack
+// (see BasesLayout), (P+1)/2 x 8 words, word (j, i) = the centred states
+// u[2j][i] (low half) and u[2j+1][i] (high half) as int16, u[j][i] =
+// x_{8j+i} - 2^(K-1), x_0 = s.
 template <int P, bool kTable>
 __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double* __restrict__ A,
                                              const uint32_t* __restrict__ Ub, uint32_t s, int K,
@@ -59,22 +59,7 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
     return z;
   };
   int32_t acc[kC];
-  if constexpr (!kTable) {
-    // the states by LFSR steps from the seed: fewer registers than the table
-    // (x - 2^(K-1) lies in [-2^23, 2^23) for K <= 24: one 24-bit multiply-add)
-    const int32_t half = int32_t(1) << (K - 1);
-#pragma unroll
-    for (int i = 0; i < kC; ++i) acc[i] = 0;
-    uint32_t x = s;
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-#pragma unroll
-      for (int i = 0; i < kC; ++i) {
-        acc[i] += __mul24(int32_t(x) - half, q[j]);
-        x = lfsr_step(x, mask);
-      }
-    }
-  } else if (K <= kPackedMaxK) {
+  if (kTable && K <= kPackedMaxK) {
     // two coefficients per dot2 (v_dot2_i32_i16)
     constexpr int PW = (P + 1) / 2;
     const uint4* src = reinterpret_cast<const uint4*>(Ub) + after(e);
@@ -92,15 +77,19 @@ __device__ __forceinline__ double exact_eval(const float (&w)[kC], const double*
         acc[i] = __builtin_amdgcn_sdot2(__builtin_bit_cast(seedq_short2, u[i]), qv, acc[i], false);
     }
   } else {
-    const uint4* src = reinterpret_cast<const uint4*>(Ub) + after(e);
+    // the states by LFSR steps from the seed (x - 2^(K-1) lies in [-2^23,
+    // 2^23) for K <= 24: one 24-bit multiply-add each)
+    const int32_t half = int32_t(1) << (K - 1);
 #pragma unroll
     for (int i = 0; i < kC; ++i) acc[i] = 0;
+    uint32_t x = s;
 #pragma unroll
     for (int j = 0; j < P; ++j) {
-      const uint4 lo = src[2 * j], hi = src[2 * j + 1];
-      const uint32_t u[kC] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
-      for (int i = 0; i < kC; ++i) acc[i] += __mul24(int32_t(u[i]), q[j]);
+      for (int i = 0; i < kC; ++i) {
+        acc[i] += __mul24(int32_t(x) - half, q[j]);
+        x = lfsr_step(x, mask);
+      }
     }
   }
   // the definition's error: index order, no fused multiply-add

@@ -67,11 +67,10 @@ constexpr float kComplementScale = 16.0f;
 // Layout of the opaque per-rung basis stack (all sections 256-byte aligned):
 //   pinv64: double [S][P][8]   pinv(U(s)), row-major per seed
 //   ub:     uint32 [S][W] the integer basis u[j][i] = x_{8j+i} - 2^(K-1) of
-//           every seed (x_0 = s), W = basis_words(K, P) words: for K <=
-//           kPackedMaxK pairs of int16 (word j*8 + i = u[2j][i] | u[2j+1][i]
-//           << 16, zero high half past P), above it int32 (word j*8 + i =
-//           u[j][i]); the exact evaluation reads it instead of stepping the
-//           LFSR
+//           every seed (x_0 = s) as pairs of int16, W = basis_words(K, P):
+//           word j*8 + i = u[2j][i] | u[2j+1][i] << 16 (zero high half past P);
+//           empty above kPackedMaxK. The P >= 5 exact evaluation reads it
+//           instead of stepping the LFSR
 //   pi16:   fp16 [ntiles][3][64][8] (empty from kComplementMinP on) 2^12 Pi_s[k]
 //           as MFMA A-operand fragments:
 //           tile T holds seeds 32T+1 .. 32T+32; fragment t, lane l, element e
@@ -85,7 +84,7 @@ constexpr float kComplementScale = 16.0f;
 // Widest LFSR whose centred states fit int16 (|x - 2^(K-1)| <= 2^(K-1)).
 constexpr int kPackedMaxK = 16;
 __host__ __device__ constexpr int basis_words(int K, int P) {
-  return K <= kPackedMaxK ? kC * ((P + 1) / 2) : kC * P;
+  return K <= kPackedMaxK ? kC * ((P + 1) / 2) : 0;
 }
 
 struct BasesLayout {
