@@ -174,6 +174,51 @@ def test_gemv_stream_matches_oracle(sq, oq, nvec):
     assert np.all(np.abs(y - ref) <= _gemv_bound(Wr, x).T + 1e-30)
 
 
+def _blocky_rungs(rng, nrows, G, R):
+    # per row, each 64-block wave step is one rung (7 in 10) or mixed; the
+    # decode-GEMV takes its one-rung path for the former
+    rob = np.empty((nrows, G), dtype=np.uint8)
+    for r in range(nrows):
+        for g0 in range(0, G, 64):
+            n = min(64, G - g0)
+            if rng.random() < 0.7:
+                rob[r, g0:g0 + n] = rng.integers(0, R)
+            else:
+                rob[r, g0:g0 + n] = rng.integers(0, R, n)
+    return rob.reshape(-1)
+
+
+@pytest.mark.parametrize("rungs", [
+    [(12, 2), (16, 3), (20, 4)],                  # leap tables at K = 12 and 16, LFSR at 20
+    [(8, 1), (13, 3), (16, 6), (23, 5), (24, 6)],  # (16, 6) past the LDS budget, K = 24
+    [(16, 6)],                                     # leap tables, P = 6
+    [(10, 5), (15, 1)],                            # leap tables, odd P
+])
+@pytest.mark.parametrize("nvec", [1, 4])
+def test_gemv_stream_one_rung_steps(sq, oq, rungs, nvec):
+    nrows, ncols = 23, 8 * 301                 # 4 full wave steps + a 45-block tail
+    nb = nrows * ncols // 8
+    rng = np.random.default_rng(len(rungs) * 10 + nvec)
+    rob = _blocky_rungs(rng, nrows, ncols // 8, len(rungs))
+    seed, exp, q = _codes(rng, rob, rungs)
+    G = ncols // 8
+    seed[2 * G + 5] = seed[11 * G + 290] = 0     # invalid seeds poison their rows
+    cnt = np.bincount(rob, minlength=len(rungs))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), rungs, nrows, ncols, _t(rob), cnt)
+    x = rng.normal(0, 1, (nvec, ncols)).astype(np.float32)
+    y = sq.gemv_stream(w, rungs, nrows, ncols, _t(x), _t(rob)).cpu().numpy()
+    K_of = np.array([rungs[r][0] for r in rob])
+    P_of = np.array([rungs[r][1] for r in rob])
+    Wr, _ = oq.decompress(np.where(seed == 0, 1, seed), exp, q, K_of, P_of)
+    Wr = np.asarray(Wr, dtype=np.float32).reshape(nrows, ncols)
+    bad = (seed == 0).reshape(nrows, -1).any(axis=1)
+    assert bad.any() and not bad.all()
+    assert np.isnan(y[:, bad]).all() and not np.isnan(y[:, ~bad]).any()
+    Wg = Wr[~bad]
+    ref = (Wg.astype(np.float64) @ x.astype(np.float64).T).T
+    assert np.all(np.abs(y[:, ~bad] - ref) <= _gemv_bound(Wg, x).T + 1e-30)
+
+
 def test_gemv_stream_invalid_block_poisons_its_row(sq):
     nrows, ncols = 6, 8 * 70
     nb = nrows * ncols // 8
