@@ -219,6 +219,29 @@ def test_gemv_stream_one_rung_steps(sq, oq, rungs, nvec):
     assert np.all(np.abs(y[:, ~bad] - ref) <= _gemv_bound(Wg, x).T + 1e-30)
 
 
+@pytest.mark.parametrize("nrows,G", [(1, 1), (3, 1), (1, 65), (2, 64), (5, 257)])
+@pytest.mark.parametrize("nvec", [1, 8])
+def test_gemv_stream_edge_shapes(sq, oq, nrows, G, nvec):
+    # one block per row, one lane of a wave step, exactly one or one past a
+    # whole step, and a step of four sub-steps plus one block
+    ncols = 8 * G
+    nb = nrows * G
+    rng = np.random.default_rng(1000 * nrows + G + nvec)
+    rob = rng.integers(0, len(MIXED), nb).astype(np.uint8)
+    seed, exp, q = _codes(rng, rob, MIXED)
+    cnt = np.bincount(rob, minlength=len(MIXED))
+    w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
+    x = rng.normal(0, 1, (nvec, ncols)).astype(np.float32)
+    y = sq.gemv_stream(w, MIXED, nrows, ncols, _t(x), _t(rob)).cpu().numpy()
+    K_of = np.array([MIXED[r][0] for r in rob])
+    P_of = np.array([MIXED[r][1] for r in rob])
+    Wr, _ = oq.decompress(seed, exp, q, K_of, P_of)
+    Wr = np.asarray(Wr, dtype=np.float32).reshape(nrows, ncols)
+    ref = (Wr.astype(np.float64) @ x.astype(np.float64).T).T
+    assert y.shape == (nvec, nrows)
+    assert np.all(np.abs(y - ref) <= _gemv_bound(Wr, x).T + 1e-30)
+
+
 def test_gemv_stream_invalid_block_poisons_its_row(sq):
     nrows, ncols = 6, 8 * 70
     nb = nrows * ncols // 8
