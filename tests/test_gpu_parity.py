@@ -284,6 +284,34 @@ def test_search_seed_chunks_match_unsplit(sq, torch, K, P):
             assert torch.equal(a, c), (K, P, label)
 
 
+@pytest.mark.parametrize("K,P", [(20, 4), (18, 3)])
+def test_search_seed_chunks_match_unsplit_many_blocks(sq, torch, K, P):
+    # the chunked walk at the rungs the multi-rung layers use, on 16 387 blocks
+    # (seven rows of 2341, a ragged last block tile): the default chunks and
+    # chunks of 512 tiles give the single walk's codes and errors bit for bit
+    import os
+    W = synthetic.weights(7, 8 * 2341, 0.02, key=700 + K, outlier_frac=0.02)
+    b = sq.build_bases(K, P)
+    d = _dev(torch, W)
+    saved = os.environ.get("SEEDQ_SEED_CHUNK_TILES")
+    out = {}
+    try:
+        for label, v in {"single walk": "0", "default": None, "chunks of 512": "512"}.items():
+            if v is None:
+                os.environ.pop("SEEDQ_SEED_CHUNK_TILES", None)
+            else:
+                os.environ["SEEDQ_SEED_CHUNK_TILES"] = v
+            out[label] = [t.cpu() for t in sq.compress(d, [b])]
+    finally:
+        if saved is None:
+            os.environ.pop("SEEDQ_SEED_CHUNK_TILES", None)
+        else:
+            os.environ["SEEDQ_SEED_CHUNK_TILES"] = saved
+    for label in out:
+        for a, c in zip(out["single walk"], out[label]):
+            assert torch.equal(a, c), (K, P, label)
+
+
 def test_search_chunks_multi_rung_match_single_walk(sq, torch):
     # a multi-rung call whose K = 17 rung is walked in sequential chunks through
     # the compaction lists: the codes must equal those of one walk per rung, bit
