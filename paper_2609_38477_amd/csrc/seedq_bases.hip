@@ -17,7 +17,8 @@
 // range basis and the vectors already chosen (twice, in fp64), the one with
 // the largest remainder taken each time (at least sqrt(remaining dims / 8)).
 // For a rank-deficient seed they span only part of the complement, which
-// keeps the screen's bound valid (a partial sum of its squares).
+// keeps the screen's bound valid (a partial sum of its squares). These rungs
+// also get pinv rounded to fp32 (see BasesLayout).
 #include "seedq_internal.h"
 
 namespace seedq {
@@ -27,7 +28,8 @@ template <int P>
 __global__ void __launch_bounds__(128)
 build_bases_kernel(int K, uint32_t mask, int64_t nseeds, double* __restrict__ pinv64,
                    uint32_t* __restrict__ ub, _Float16* __restrict__ pi16, _Float16* __restrict__ nc16,
-                   int32_t* __restrict__ U_out, float* __restrict__ pinv_out) {
+                   float* __restrict__ pinv32, int32_t* __restrict__ U_out,
+                   float* __restrict__ pinv_out) {
   constexpr int M = complement_dims(P);
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   // fragment address of pair k for this seed (see BasesLayout)
@@ -227,6 +229,7 @@ build_bases_kernel(int K, uint32_t mask, int64_t nseeds, double* __restrict__ pi
 #pragma unroll
       for (int j = 0; j < P; ++j) v = fma(V[p][j] * inv2[j], A[i][j], v);
       P64[p * kC + i] = v;
+      if constexpr (M > 0) pinv32[idx * (P * kC) + p * kC + i] = float(v);
       if (pinv_out) pinv_out[(int64_t(p) * nseeds + idx) * kC + i] = float(v);
     }
   }
@@ -243,7 +246,8 @@ hipError_t launch_p(int K, int64_t nseeds, void* d_bases, int32_t* d_U, float* d
                      lfsr_mask(K), nseeds, reinterpret_cast<double*>(base + L.off_pinv64),
                      reinterpret_cast<uint32_t*>(base + L.off_ub),
                      reinterpret_cast<_Float16*>(base + L.off_pi16),
-                     reinterpret_cast<_Float16*>(base + L.off_nc16), d_U, d_pinv);
+                     reinterpret_cast<_Float16*>(base + L.off_nc16),
+                     reinterpret_cast<float*>(base + L.off_pinv32), d_U, d_pinv);
   return hipGetLastError();
 }
 

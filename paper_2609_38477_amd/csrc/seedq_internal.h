@@ -81,6 +81,9 @@ constexpr float kComplementScale = 16.0f;
 //           range(U(s)), c < M; fragment c of tile T, lane l, element e is
 //           hi(2^4 n_c[e]) for l < 32 and lo(2^4 n_c[e]) = fp16(2^4 n_c[e] -
 //           hi) for l >= 32, of seed 32T + (l % 32) + 1 (zero beyond 2^K - 1)
+//   pinv32: float [S][P][8] (empty below kComplementMinP): pinv64 rounded to
+//           fp32, from which the many evaluations of these rungs decide their
+//           exponent and mantissas when the rounding provably cannot matter
 // Widest LFSR whose centred states fit int16 (|x - 2^(K-1)| <= 2^(K-1)).
 constexpr int kPackedMaxK = 16;
 __host__ __device__ constexpr int basis_words(int K, int P) {
@@ -89,7 +92,7 @@ __host__ __device__ constexpr int basis_words(int K, int P) {
 
 struct BasesLayout {
   int64_t nseeds, ntiles;
-  size_t off_pinv64, off_ub, off_pi16, off_nc16, total;
+  size_t off_pinv64, off_ub, off_pi16, off_nc16, off_pinv32, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -102,7 +105,9 @@ inline BasesLayout bases_layout(int K, int P) {
   L.off_ub = align256(L.off_pinv64 + size_t(L.nseeds) * P * kC * sizeof(double));
   L.off_pi16 = align256(L.off_ub + size_t(L.nseeds) * basis_words(K, P) * sizeof(uint32_t));
   L.off_nc16 = align256(L.off_pi16 + (complement_dims(P) > 0 ? 0 : size_t(L.ntiles) * kTileBytes));
-  L.total = align256(L.off_nc16 + size_t(L.ntiles) * complement_dims(P) * 64 * kC * 2);
+  L.off_pinv32 = align256(L.off_nc16 + size_t(L.ntiles) * complement_dims(P) * 64 * kC * 2);
+  L.total = align256(L.off_pinv32 +
+                     (complement_dims(P) > 0 ? size_t(L.nseeds) * P * kC * sizeof(float) : 0));
   return L;
 }
 

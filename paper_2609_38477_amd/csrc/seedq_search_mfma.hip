@@ -151,6 +151,7 @@ struct MfmaArgs {
   int K;
   uint32_t mask;
   const uint32_t* ub;
+  const float* pinv32;
   const double* pinv64;
   const half8* pi16;
   int64_t ntiles;
@@ -307,10 +308,10 @@ typedef __fp16 fp16x2 __attribute__((ext_vector_type(2)));
 
 template <int P>
 __global__ void __launch_bounds__(kWaves * 64)
-__attribute__((amdgpu_waves_per_eu(half_records(P) ? 4 : 3)))
+__attribute__((amdgpu_waves_per_eu(3)))
 search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* __restrict__ list,
                    const int32_t* __restrict__ off, int rung, int K, uint32_t mask,
-                   const uint32_t* __restrict__ ub,
+                   const uint32_t* __restrict__ ub, const float* __restrict__ pinv32,
                    const double* __restrict__ pinv64, const half8* __restrict__ pi16,
                    int64_t ntiles, float one_minus_gamma, uint32_t* __restrict__ seed_out,
                    uint8_t* __restrict__ exp_out, int8_t* __restrict__ q_out,
@@ -468,7 +469,13 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
           float w[kC];
           load_block(W, b, true, w);
           int qe, q[P];
-          err = exact_eval<P, (M > 0)>(w, pinv64 + int64_t(seed - 1) * (P * kC),
+          if constexpr (M > 0)
+            err = exact_eval_f32<P>(w, pinv32 + int64_t(seed - 1) * (P * kC),
+                                    pinv64 + int64_t(seed - 1) * (P * kC),
+                                    ub + int64_t(seed - 1) * basis_words(K, P), seed, K, mask, qe,
+                                    q);
+          else
+            err = exact_eval<P, false>(w, pinv64 + int64_t(seed - 1) * (P * kC),
                                        ub + int64_t(seed - 1) * basis_words(K, P), seed, K, mask,
                                        qe, q);
           if (ent & kFinal) {
@@ -1164,6 +1171,7 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
   a.mask = lfsr_mask(K);
   a.ub = reinterpret_cast<const uint32_t*>(base + L.off_ub);
   a.pinv64 = reinterpret_cast<const double*>(base + L.off_pinv64);
+  a.pinv32 = complement_dims(P) > 0 ? reinterpret_cast<const float*>(base + L.off_pinv32) : nullptr;
   a.pi16 = reinterpret_cast<const half8*>(base + (complement_dims(P) > 0 ? L.off_nc16 : L.off_pi16));
   a.ntiles = L.ntiles;
   const double gamma = std::sqrt(double(P)) * 0x1p-10 * (1.0 + 0x1p-6) + 0x1p-14;
@@ -1190,7 +1198,8 @@ hipError_t launch_mfma_p(const float* d_W, int64_t nblocks, const int32_t* d_lis
                          a.err_out, int(nseq), int(c), carry);
     } else {
       hipLaunchKernelGGL(search_mfma_kernel<P>, grid, dim3(kWaves * 64), 0, stream,
-                         a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.ub, a.pinv64, a.pi16,
+                         a.W, a.nblocks, a.list, a.off, a.rung, a.K, a.mask, a.ub, a.pinv32,
+                         a.pinv64, a.pi16,
                          a.ntiles, a.one_minus_gamma, a.seed_out, a.exp_out, a.q_out, a.err_out,
                          int(nseq), int(c), carry);
     }

@@ -383,6 +383,36 @@ def test_search_dense_survivor_rungs(sq, oq, torch, K, P, nb):
                  q.cpu().numpy(), err.cpu().numpy(), f"K{K}P{P}")
 
 
+@pytest.mark.parametrize("K,P", [(10, 5), (11, 6), (16, 6)])
+def test_search_near_rounding_boundaries(sq, oq, torch, K, P):
+    # blocks within 1e-6 of the span of one seed's basis, U(s) t plus noise,
+    # with t_0 2^e a half-integer and the other t_p 2^e integers: the seed's
+    # first mantissa lies within the fp32 evaluation's error of its rounding
+    # boundary (about 1e-4 in units of 2^-e), so these rungs' fp32 decision is
+    # not trusted there and the fp64 one is taken; the noise moves t_0 2^e off
+    # the half-integer by far more than fp64's error (U t 2^-e alone is exact in
+    # fp32 and would make an exact tie, which fp64 roundings may break either
+    # way), so the fp64 decision is unambiguous and the codes must be the
+    # oracle's
+    rng = np.random.default_rng(900 + K + P)
+    nb = 96
+    blocks = np.zeros((nb, 8), np.float32)
+    for b in range(nb):
+        s = int(rng.integers(1, 1 << K))
+        e = int(rng.integers(3, 6))
+        k = rng.integers(4, 8, P) * rng.choice([-1, 1], P)
+        t = k.astype(np.float64)
+        t[0] = 5.5 if rng.random() < 0.5 else -5.5   # e + 1 cannot fit: 2 |t_0| > 8.5
+        w = oq.basis(K, P, s) @ (t * 2.0 ** -e)
+        w += 1e-6 * np.sqrt(np.mean(w * w)) * rng.standard_normal(8)
+        blocks[b] = w.astype(np.float32)
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(_dev(torch, blocks.reshape(1, -1)), [b])
+    torch.cuda.synchronize()
+    check_search(oq, blocks, K, P, seed.cpu().numpy().view(np.uint32), e.cpu().numpy(),
+                 q.cpu().numpy(), err.cpu().numpy(), f"boundary K{K}P{P}")
+
+
 @pytest.mark.parametrize("K,P", [(11, 5), (11, 6), (13, 6)])
 def test_search_rank_deficient_seeds_complement(sq, oq, torch, K, P):
     # blocks in (or next to) the column span of the rank-deficient seeds of a
