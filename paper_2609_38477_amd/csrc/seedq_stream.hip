@@ -385,8 +385,12 @@ row_bits_kernel(const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, i
 
 constexpr int kGemvNB = 4;  // sub-steps of 64 blocks per wave step
 
+// The kernel is bound by issue latency, not bytes: more resident waves hide
+// more of it. One vector fits 64 VGPRs (8 waves per SIMD) and four fit 96 (5
+// waves) without spilling; eight keep the compiler's choice.
 template <int NV>
 __global__ void __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(NV == 1 ? 8 : (NV == 4 ? 5 : 1))))
 gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
                    const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
                    const int64_t* __restrict__ row_off, const float* __restrict__ x,
