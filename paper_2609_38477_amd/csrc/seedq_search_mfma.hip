@@ -284,24 +284,34 @@ SEEDQ_INLINE uint32_t lane_now() {
 constexpr uint32_t kFinal = 0x80u;
 static_assert(kSlots <= 128, "slot must fit 7 bits");
 
-// Walk survivors of the P <= 3 kernel are first kept as records: a lane whose
-// fold passes stores its 16 bounds with the seed tile, its half and the block
-// slot (one 64-byte row and one meta word in LDS; meta = tile << 8 | half << 7
-// | slot). Records become candidates 64 at a time, each compared with its
-// block's threshold of that moment, so the per-seed ballots run once per 64
-// records instead of once per passing block tile, and records whose block has
+// Walk survivors of this kernel are first kept as records: a lane whose fold
+// passes stores its 16 bounds with the seed tile, its half and the block slot
+// (one row and one meta word in LDS; meta = tile << 8 | half << 7 | slot).
+// Records become candidates 64 at a time, each compared with its block's
+// threshold of that moment, so the per-seed ballots run once per 64 records
+// instead of once per passing block tile, and records whose block has
 // meanwhile found a better code drop out before the exact evaluation.
-constexpr int kRecFlush = 32;                 // records waiting after a pair of block tiles
-constexpr int kRecCap = kRecFlush + 64;       // one block tile adds at most 64
+// At P >= 5, where several hundred seeds per block survive the screen, the
+// records wait until 64 of them fill a round (kRecRoundMin; the rest wait for
+// the next call) and a round's passing bounds are compacted by a prefix sum
+// over the lanes instead of one ballot and branch per seed row (measured on
+// 2.1 M blocks: (16,6) 9-10 % and (13..16,5) 6-10 % faster than per-row
+// ballots over rounds of 32-64).
+template <int P>
+constexpr int kRecFlush = complement_dims(P) > 0 ? 64 : 32;   // records waiting after a pair
+template <int P>
+constexpr int kRecCap = kRecFlush<P> + 64;   // one block tile adds at most 64
+template <int P>
+constexpr int kRecRoundMin = complement_dims(P) > 0 ? 64 : 1;
 constexpr int kQCapRec = 64 + 64 * 16;        // < 64 waiting + one round of 64 records
-// At P = 6 (two complement vectors) records hold their bounds as fp16 (16 x
-// 2 bytes: two float4 of storage instead of four), which brings the kernel's
-// LDS to 40 KB and, with at most 128 VGPRs, four waves per SIMD (measured on
-// 2.1 M blocks: (14..16,6) 5-6 % faster; at P = 5 the register limit spills
-// and measured 18 % slower). The values -sum d^2 lie in fp16's range (|sum
-// d^2| < 2^13 with the complement operand's 2^4 scale) and are rounded toward
-// zero, i.e. up, so that a stored bound is never below the computed one.
-__host__ __device__ constexpr bool half_records(int P) { return complement_dims(P) == 2; }
+// At P >= 5 (complement screen) records hold their bounds as fp16 (16 x 2
+// bytes: two float4 of storage instead of four), which keeps the kernel's LDS
+// at 44 KB with 128 records per wave, three workgroups per CU. The values
+// -sum d^2 lie in fp16's range (sum d^2 <= 2^8 ||w||^2 < 2^13: the complement
+// operand carries 2^4 and the block's power-of-two scaling leaves every |w_i|
+// below 2) and are rounded toward zero, i.e. up, so that a stored bound is
+// never below the computed one.
+__host__ __device__ constexpr bool half_records(int P) { return complement_dims(P) > 0; }
 template <int P>
 constexpr int kRecVecs = half_records(P) ? 2 : 4;
 typedef __fp16 fp16x2 __attribute__((ext_vector_type(2)));
@@ -323,9 +333,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
   // power-of-two scaling of the block: ilogb of its largest |w_i|, down to -149
   // for fp32 subnormals, so 16 bits
   __shared__ int16_t ex_all[kWaves][kSlots];
-  // 16 bounds per record: fp32, or fp16 at P = 6 (see half_records)
-  __shared__ float4 rec_all[kWaves][kRecCap][kRecVecs<P>];
-  __shared__ uint32_t meta_all[kWaves][kRecCap];
+  // 16 bounds per record: fp32, or fp16 at P >= 5 (see half_records)
+  __shared__ float4 rec_all[kWaves][kRecCap<P>][kRecVecs<P>];
+  __shared__ uint32_t meta_all[kWaves][kRecCap<P>];
   __shared__ uint32_t queue_all[kWaves][kQCapRec];
 
   const int lane = threadIdx.x & 63;
@@ -503,12 +513,13 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
 
   int nrec = 0;  // wave-uniform
   // Records -> candidates: lane l takes record base + l of the top 64 and
-  // compares its 16 bounds with the block's current threshold; one ballot per
-  // seed row queues the passing seeds. Full batches are evaluated after each
-  // round of records; the walk's thresholds are refreshed at the end.
-  auto process = [&]() __attribute__((always_inline)) {
+  // compares its 16 bounds with the block's current threshold; the passing
+  // seeds are queued. Rounds run while at least min_round records wait. Full
+  // batches are evaluated after each round of records; the walk's thresholds
+  // are refreshed at the end.
+  auto process = [&](int min_round) __attribute__((always_inline)) {
     __threadfence_block();
-    while (nrec > 0) {
+    while (nrec >= min_round && nrec > 0) {
       const int e = nrec < 64 ? nrec : 64;
       const int base = nrec - e;
       const bool live = lane < e;
@@ -548,16 +559,45 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       const uint32_t seedbase = (m >> 8) * 32u + 1u;
       const int hh = int((m >> 7) & 1u);
       const uint32_t slot = m & 0x7Fu;
+      if constexpr (M > 0) {
+        // the lane's passing bounds as a mask (t = +inf on lanes without a
+        // record), the exclusive prefix sum of their counts over the wave (by
+        // the counts' five bit planes), then one queued seed per lane and step
+        uint32_t pm = 0u;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const bool pass = bnd[j] >= t;   // t = +inf on lanes without a record
-        const uint64_t mk = ballot(pass);
-        if (mk != 0ull) {
-          if (pass) {
-            const uint32_t seed = seed_of(seedbase, j, hh);
-            queue[qcount + lanes_below(mk)] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
+        for (int j = 0; j < 16; ++j) pm |= (bnd[j] >= t ? 1u : 0u) << j;
+        const uint32_t cnt = uint32_t(__builtin_popcount(pm));
+        uint32_t off = uint32_t(qcount);
+        int total = 0;
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+          const uint64_t mk = ballot(((cnt >> k) & 1u) != 0u);
+          off += uint32_t(lanes_below(mk)) << k;
+          total += __popcll(mk) << k;
+        }
+        while (ballot(pm != 0u) != 0ull) {
+          if (pm != 0u) {
+            // seed_of for the lowest set row j
+            const uint32_t j = uint32_t(__builtin_ctz(pm));
+            const uint32_t seed = seedbase + 8u * (j >> 2) + 4u * uint32_t(hh) + (j & 3u);
+            queue[off] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
+            ++off;
+            pm &= pm - 1u;
           }
-          qcount += __popcll(mk);
+        }
+        qcount += total;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const bool pass = bnd[j] >= t;   // t = +inf on lanes without a record
+          const uint64_t mk = ballot(pass);
+          if (mk != 0ull) {
+            if (pass) {
+              const uint32_t seed = seed_of(seedbase, j, hh);
+              queue[qcount + lanes_below(mk)] = ((seed <= nseeds ? seed : 0u) << 8) | slot;
+            }
+            qcount += __popcll(mk);
+          }
         }
       }
       nrec = base;
@@ -645,9 +685,9 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
       const uint64_t m0 = ballot(p0), m1 = ballot(p1);
       if ((m0 | m1) != 0ull) {
         record(2 * pr, acc0, p0, m0, t32);
-        if (nrec > kRecCap - 64) process();
+        if (nrec > kRecCap<P> - 64) process(kRecRoundMin<P>);
         record(2 * pr + 1, acc1, p1, m1, t32);
-        if (nrec >= kRecFlush) process();
+        if (nrec >= kRecFlush<P>) process(kRecRoundMin<P>);
       }
     }
   };
@@ -675,7 +715,7 @@ search_mfma_kernel(const float* __restrict__ W, int64_t nblocks, const int32_t* 
     }
     if (T + 1 < T1) tile(y, T + 1);
   }
-  process();
+  process(1);
   evaluate(1);
 
   // ---------------------------------------------------------------- results

@@ -160,6 +160,31 @@ def test_search_edge_blocks(sq, oq, torch):
     assert np.array_equal(seed, ref.seed)
 
 
+@pytest.mark.parametrize("K,P", [(10, 5), (10, 6), (12, 5), (12, 6)])
+def test_search_edge_blocks_complement(sq, oq, torch, K, P):
+    # degenerate blocks at the complement-screen rungs, most of them blocks whose
+    # seeds all tie exactly (fp32 subnormals: every code is q = 0 and every
+    # error is ||w||^2), in whole block tiles: every bound of every record then
+    # passes, the largest queue a round of records can fill (16 seeds per
+    # record); the rest as in test_search_edge_blocks plus ordinary blocks
+    rng = np.random.default_rng(11)
+    tie = [np.full(8, 1e-39), np.full(8, 1.4e-45), rng.uniform(-1, 1, 8) * 1e-42,
+           rng.normal(0, 1e-40, 8)]
+    blocks = [tie[i % len(tie)] for i in range(192)]
+    blocks += [np.zeros(8), rng.normal(0, 1e-30, 8), rng.normal(0, 1e15, 8),
+               np.array([1, 0, 0, 0, 0, 0, 0, 0.0]), np.full(8, 0.02),
+               rng.normal(0, 0.02, 8) * np.array([1, 1, 1, 1e3, 1, 1, 1, 1])]
+    blocks += [rng.normal(0, 0.02, 8) for _ in range(58)]
+    W = np.array(blocks, dtype=np.float32).reshape(1, -1)
+    b = sq.build_bases(K, P)
+    seed, e, q, err = sq.compress(_dev(torch, W), [b])
+    torch.cuda.synchronize()
+    seed, e, q, err = seed.cpu().numpy().view(np.uint32), e.cpu().numpy(), q.cpu().numpy(), err.cpu().numpy()
+    assert np.all(seed[:192] == 1) and not q[:192].any()
+    ref = check_search(oq, W, K, P, seed, e, q, err, f"edge K{K}P{P}")
+    assert np.array_equal(seed, ref.seed)
+
+
 def test_search_single_block(sq, oq, torch):
     W = synthetic.weights(1, 8, 0.02, key=77)
     b = sq.build_bases(12, 3)
