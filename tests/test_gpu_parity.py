@@ -309,6 +309,41 @@ def test_search_seed_chunks_match_unsplit(sq, torch, K, P):
             assert torch.equal(a, c), (K, P, label)
 
 
+@pytest.mark.parametrize("K,P", [(12, 5), (13, 6)])
+def test_search_seed_chunks_carry_ties(sq, oq, torch, K, P):
+    # blocks whose seeds all tie (fp32 subnormals) beside ordinary ones, the
+    # walk cut into chunks of 8 tiles: every later chunk meets the first
+    # chunk's best error exactly again, and the carried best seed must stay the
+    # smallest (seed 1); every chunk length gives the single walk's codes, and
+    # those are the oracle's
+    import os
+    rng = np.random.default_rng(23)
+    tie = [np.full(8, 1e-39), rng.uniform(-1, 1, 8) * 1e-42]
+    blocks = [tie[i % 2] for i in range(96)] + [rng.normal(0, 0.02, 8) for _ in range(64)]
+    W = np.array(blocks, dtype=np.float32).reshape(1, -1)
+    b = sq.build_bases(K, P)
+    d = _dev(torch, W)
+    saved = os.environ.get("SEEDQ_SEED_CHUNK_TILES")
+    out = {}
+    try:
+        for v in ("0", "8", "32"):
+            os.environ["SEEDQ_SEED_CHUNK_TILES"] = v
+            out[v] = [t.cpu() for t in sq.compress(d, [b])]
+    finally:
+        if saved is None:
+            os.environ.pop("SEEDQ_SEED_CHUNK_TILES", None)
+        else:
+            os.environ["SEEDQ_SEED_CHUNK_TILES"] = saved
+    for v in ("8", "32"):
+        for a, c in zip(out["0"], out[v]):
+            assert torch.equal(a, c), (K, P, v)
+    seed, e, q, err = (t.numpy() for t in out["8"])
+    seed = seed.view(np.uint32)
+    assert np.all(seed[:96] == 1)
+    ref = check_search(oq, W, K, P, seed, e, q, err, f"chunk ties K{K}P{P}")
+    assert np.array_equal(seed, ref.seed)
+
+
 @pytest.mark.parametrize("K,P", [(20, 4), (18, 3)])
 def test_search_seed_chunks_match_unsplit_many_blocks(sq, torch, K, P):
     # the chunked walk at the rungs the multi-rung layers use, on 16 387 blocks
