@@ -335,8 +335,12 @@ int seedq_decompress_stream(const uint32_t* d_stream, size_t stream_bytes,
  * sides, W_hat decoded on the fly and never stored (the codec's bandwidth
  * motivation, section 1; per the appendix on cost the decoder regenerates the
  * LFSR states and does P multiply-adds for each weight). Every weight is the one
- * seedq_decompress_stream would write; the products are accumulated in fp32,
- * each lane over every 64th block of the row, then a tree across the lanes.
+ * seedq_decompress_stream would write; the products are accumulated in fp32:
+ * for 1, 2 or 4 vectors each lane over every 64th block of the row, then a tree
+ * across the lanes; for 8 on the matrix core, each 64-block step of the row
+ * split in 16 shares of 4 blocks, a share's products in 8 chained four-term
+ * accumulations, the steps added share by share, then the 16 shares summed in
+ * a fixed order.
  *   nvec:  1, 2, 4 or 8.
  *   d_x:   device fp32 [nvec][ncols], 16-byte aligned.
  *   d_y:   device fp32 [nvec][nrows] out.

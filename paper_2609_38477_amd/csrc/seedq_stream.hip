@@ -387,7 +387,8 @@ constexpr int kGemvNB = 4;  // sub-steps of 64 blocks per wave step
 
 // The kernel is bound by issue latency, not bytes: more resident waves hide
 // more of it. One vector fits 64 VGPRs (8 waves per SIMD) and four fit 96 (5
-// waves) without spilling; eight keep the compiler's choice.
+// waves) without spilling; two keep the compiler's choice. (Eight vectors go
+// to gemv_stream_tile_kernel below.)
 template <int NV>
 __global__ void __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(NV == 1 ? 8 : (NV == 4 ? 5 : 1))))
@@ -462,6 +463,120 @@ gemv_stream_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
     if (lane == 0) y[v * ldy + r] = t;
+  }
+}
+
+// Decode-GEMV for eight vectors with the products on the matrix core
+// (v_mfma_f32_16x16x4_f32). A workgroup of 16 waves takes 16 rows, one wave
+// per row decoding 64 consecutive blocks per step exactly as the one-vector
+// kernel does (one block per lane, offsets by a wave prefix sum), into a
+// 16-row tile of weights in LDS (two buffers, one barrier per step). Then
+// wave w multiplies the tile's blocks 4w .. 4w + 3 by the vectors: product m
+// takes A[i][k] = weight m of block 4w + k of row i and B[k][n] = x_n at the
+// same column, so that lane (i, k) reads 8 consecutive weights of the tile and
+// lane (k, n) 8 consecutive entries of x_n. The 16 waves' partial products are
+// summed in a fixed order at the end. Rounding: a product passes through at
+// most 8 matrix-core accumulations of a step (5 + 7 x 4 roundings), one
+// addition per step and the 16-way sum (15). The decode costs the same as in
+// the one-vector kernel, so this pays where that kernel's per-vector
+// multiply-adds outweigh the tile's barrier and LDS traffic: on an 8192 x 28672
+// layer 0.26 against 0.35 ms at eight vectors, but 0.27 against 0.23 at four.
+constexpr int kTlRows = 16;
+constexpr int kTlBlocks = 64;                  // blocks per row and step
+constexpr int kTlStride = kTlBlocks * kC + 4;  // floats per tile row (padded)
+typedef float tl_floatx4 __attribute__((ext_vector_type(4)));
+
+template <int NV>
+__global__ void __launch_bounds__(64 * kTlRows)
+gemv_stream_tile_kernel(const uint32_t* __restrict__ stream, int64_t nwords,
+                        const uint8_t* __restrict__ rung, RungTable rt, int64_t nrows, int64_t G,
+                        const int64_t* __restrict__ row_off, const float* __restrict__ x,
+                        int64_t ldx, float* __restrict__ y, int64_t ldy) {
+  static_assert(NV >= 1 && NV <= 16, "one B column per vector");
+  static_assert(kTlRows * 4 == kTlBlocks, "each wave multiplies 4 blocks of the tile");
+  __shared__ uint4 tab[kRungTable];
+  __shared__ __attribute__((aligned(16))) float tile[2][kTlRows][kTlStride];
+  fill_rung_table(tab, rt);
+  __syncthreads();
+  const int wave = int(threadIdx.x >> 6), lane = int(threadIdx.x & 63);
+  const int i = lane & 15, k = lane >> 4;
+  const int64_t r = int64_t(blockIdx.x) * kTlRows + wave;   // the row this wave decodes
+  const bool row_ok = r < nrows;
+  const uint32_t nr = uint32_t(rt.n);
+  const uint8_t* row = rung && row_ok ? rung + r * G : nullptr;
+  int64_t run = row_ok ? row_off[r] : 0;
+  tl_floatx4 sum = {0.f, 0.f, 0.f, 0.f};
+  int buf = 0;
+  for (int64_t g0 = 0; g0 < G; g0 += kTlBlocks) {   // the same trip count in every wave
+    // decode block g0 + lane of row r into the tile
+    const int64_t g = g0 + lane;
+    const bool in = row_ok && g < G;
+    const uint4 info = in ? tab[table_index(row ? uint32_t(row[g]) : 0u, nr)]
+                          : make_uint4(0u, 0u, 0u, 0u);
+    uint64_t tot;
+    const uint64_t ex = wave_exclusive_scan64(uint64_t(info.w), &tot);
+    const int64_t pos = run + int64_t(ex);
+    run += int64_t(tot);
+    float f[kC];
+#pragma unroll
+    for (int e2 = 0; e2 < kC; ++e2) f[e2] = 0.f;
+    if (in) {
+      const int K = int(info.x), P = int(info.y);
+      uint32_t lo = 0u, hi = 0u;
+      bool ok = read_window(stream, nwords, pos, info.w, lo, hi);
+      const uint32_t sd = lo & ((1u << K) - 1u);
+      const int e = int((lo >> K) & 15u);
+      const uint32_t qb = __builtin_amdgcn_alignbit(hi, lo, uint32_t(K + 4));
+      ok = ok && sd != 0u;
+      int32_t a8[kC];
+      block_acc_q(ok ? sd : 1u, K, P, info.z,
+                  [&](int j) { return __builtin_amdgcn_sbfe(int32_t(qb), 4 * j, 4); }, a8);
+      const int sc = -(K - 1 + e);
+#pragma unroll
+      for (int e2 = 0; e2 < kC; ++e2)
+        f[e2] = ok ? ldexpf(__int2float_rn(a8[e2]), sc) : __int_as_float(0x7fc00000);
+    }
+    float4* dst = reinterpret_cast<float4*>(&tile[buf][wave][lane * kC]);
+    dst[0] = make_float4(f[0], f[1], f[2], f[3]);
+    dst[1] = make_float4(f[4], f[5], f[6], f[7]);
+    __syncthreads();
+    // blocks gb = g0 + 4 wave + k of the 16 rows against the vectors
+    const int64_t gb = g0 + 4 * wave + k;
+    const float4* src = reinterpret_cast<const float4*>(&tile[buf][i][(4 * wave + k) * kC]);
+    const float4 a0 = src[0], a1 = src[1];
+    float4 b0 = make_float4(0.f, 0.f, 0.f, 0.f), b1 = b0;
+    if (i < NV && gb < G) {
+      const float4* xv = reinterpret_cast<const float4*>(x + i * ldx + gb * kC);
+      b0 = xv[0];
+      b1 = xv[1];
+    }
+    tl_floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, b0.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, b0.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, b0.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, b0.w, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, b1.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, b1.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, b1.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, b1.w, acc, 0, 0, 0);
+    sum += acc;
+    buf ^= 1;
+  }
+  // lane l of wave w holds rows 4 (l / 16) + v, vector l % 16; the 16 waves'
+  // sums go through the (no longer read) tile
+  __syncthreads();
+  float* part = &tile[0][0][0];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) part[(wave * 4 + v) * 64 + lane] = sum[v];
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      float t = part[v * 64 + lane];
+      for (int w = 1; w < kTlRows; ++w) t += part[(w * 4 + v) * 64 + lane];
+      const int64_t rr = int64_t(blockIdx.x) * kTlRows + 4 * k + v;
+      if (i < NV && rr < nrows) y[i * ldy + rr] = t;
+    }
   }
 }
 
@@ -541,8 +656,9 @@ hipError_t launch_gemv_stream(const uint32_t* d_stream, int64_t nwords, const ui
                          nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
       break;
     case 8:
-      hipLaunchKernelGGL(gemv_stream_kernel<8>, dim3(grid), dim3(kThreads), 0, stream, d_stream,
-                         nwords, d_rung, rt, nrows, G, row_off, d_x, ldx, d_y, ldy);
+      hipLaunchKernelGGL(gemv_stream_tile_kernel<8>, dim3(unsigned((nrows + kTlRows - 1) / kTlRows)),
+                         dim3(64 * kTlRows), 0, stream, d_stream, nwords, d_rung, rt, nrows, G,
+                         row_off, d_x, ldx, d_y, ldy);
       break;
     default:
       return hipErrorInvalidValue;

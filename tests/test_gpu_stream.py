@@ -146,11 +146,16 @@ def test_decoder_path_with_rederived_rungs(sq):
 
 
 def _gemv_bound(W, x):
-    # fp32 accumulation: every lane adds at most 4 ceil(G / 256) block partials
-    # (G = ncols / 8), each a chain of 8 fused products, then a 6-level tree; the
-    # bound used, (8 ceil(G / 64) + 8) u sum |w||x|, is above that term count
+    # fp32 accumulation, by the kernel that runs for x's number of vectors
+    # (G = ncols / 8). Up to four: a lane adds at most ceil(G / 64) block
+    # partials, each a chain of 8 fused products, then a 6-level tree: bound
+    # (8 ceil(G / 64) + 8) u sum |w||x|. Eight (matrix core): a product passes
+    # through at most 8 accumulations of 4 products in its 64-block step
+    # (1 + 4 + 7 x 4 roundings), one addition per step and a sum of 16:
+    # (50 + ceil(G / 64)) u sum |w||x|
     ncols = W.shape[1]
-    n = (ncols // 8 + 63) // 64 * 8 + 8
+    G = ncols // 8
+    n = 50 + (G + 63) // 64 if x.shape[0] >= 8 else (G + 63) // 64 * 8 + 8
     return n * 2.0 ** -24 * (np.abs(W.astype(np.float64)) @ np.abs(x.astype(np.float64)).T)
 
 
