@@ -199,7 +199,7 @@ def _blocky_rungs(rng, nrows, G, R):
     [(16, 6)],                                     # leap tables, P = 6
     [(10, 5), (15, 1)],                            # leap tables, odd P
 ])
-@pytest.mark.parametrize("nvec", [1, 4])
+@pytest.mark.parametrize("nvec", [1, 4, 8])
 def test_gemv_stream_one_rung_steps(sq, oq, rungs, nvec):
     nrows, ncols = 23, 8 * 301                 # 4 full wave steps + a 45-block tail
     nb = nrows * ncols // 8
@@ -247,7 +247,8 @@ def test_gemv_stream_edge_shapes(sq, oq, nrows, G, nvec):
     assert np.all(np.abs(y - ref) <= _gemv_bound(Wr, x).T + 1e-30)
 
 
-def test_gemv_stream_invalid_block_poisons_its_row(sq):
+@pytest.mark.parametrize("nvec", [1, 8])
+def test_gemv_stream_invalid_block_poisons_its_row(sq, nvec):
     nrows, ncols = 6, 8 * 70
     nb = nrows * ncols // 8
     rng = np.random.default_rng(77)
@@ -257,9 +258,9 @@ def test_gemv_stream_invalid_block_poisons_its_row(sq):
     valid = rob < len(MIXED)
     cnt = np.bincount(rob[valid], minlength=len(MIXED))
     w = sq.pack(_t(seed.view(np.int32)), _t(exp), _t(q), MIXED, nrows, ncols, _t(rob), cnt)
-    x = rng.normal(0, 1, ncols).astype(np.float32)
-    y = sq.gemv_stream(w, MIXED, nrows, ncols, _t(x), _t(rob)).cpu().numpy()
-    assert np.isnan(y[3]) and not np.isnan(np.delete(y, 3)).any()
+    x = rng.normal(0, 1, (nvec, ncols)).astype(np.float32)
+    y = sq.gemv_stream(w, MIXED, nrows, ncols, _t(x), _t(rob)).cpu().numpy().reshape(nvec, nrows)
+    assert np.isnan(y[:, 3]).all() and not np.isnan(np.delete(y, 3, axis=1)).any()
 
 
 def test_gemv_stream_full_size(sq):
